@@ -1,0 +1,190 @@
+/*
+ * vbq.h -- C ABI of libvbq: packed variable-bit-width weights (VBQ) and the
+ * fused dequantize-and-multiply used by autoregressive decode, for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * Method (arxiv 2607.02893, "Variable Bit-width Quantization"):
+ *   - A weight matrix W[N][K] is cut into contiguous groups of G = 64 weights
+ *     along K.  Group g has its own bit-width b_g in {1,2,4,8} and its own
+ *     scale s_g (paper section 3.1).
+ *   - b >= 2 (paper Eq. (1)): symmetric absmax,
+ *       s = max|w| / (2^(b-1)-1),  q = clip(round(w/s), -(2^(b-1)-1), 2^(b-1)-1),
+ *       w_hat = s*q.
+ *   - b = 1 (paper section 3.1, text after Eq. (1)): w_hat = sign(w) * mean|w|.
+ *   - Decode streams the packed low-bit codes, expands them in registers with
+ *     the group scale and accumulates the matrix-vector product; the
+ *     full-precision matrix is never materialised (paper section 6, "Fused
+ *     kernels over packed weights").
+ *
+ * Readings fixed by this library where the paper is silent:
+ *   - round() is round-half-to-even; the codes are computed against the scale
+ *     AFTER it has been rounded to fp16 (so quantize(dequantize(q)) == q).
+ *   - scales are IEEE fp16, computed in double and rounded once (RNE).
+ *   - sign(0) = +1 for the 1-bit rule (also for -0.0).
+ *   - the 1-bit absmean is the sequential double sum over the 64 weights / 64.
+ *   - an all-zero group at b >= 2 has s = 0 and q = 0.
+ *   - the level set of width b >= 2 is {-(2^(b-1)-1) .. 2^(b-1)-1}; the code
+ *     for -2^(b-1) is never produced and is rejected by vbq_pack_codes.
+ *   - K must be a multiple of 64 (a partial group would change the 1-bit mean).
+ *   - products are accumulated in fp32; y is fp32.
+ *
+ * ---------------------------------------------------------------------------
+ * Packed layout, version 1 (the paper leaves the storage format open; this is
+ * the format every entry point below reads or writes)
+ * ---------------------------------------------------------------------------
+ *   G   = K/64 group columns.  Class c = log2(b): 0:1-bit 1:2-bit 2:4-bit 3:8-bit.
+ *   R   = tile_rows (power of two in [16,256]); T = ceil(N/R) row tiles.
+ *   C   = chunk_groups (1..128, R*C <= 8192); U = ceil(G/C) column chunks.
+ *   Unit (t,k), u = t*U + k, covers rows [tR, min(N,tR+R)) and group columns
+ *   [kC, min(G,kC+C)).  Inside a unit, position p = (j-kC)*R + (r-tR) for
+ *   group column j and row r ("column-major"; the stride is R even in the last,
+ *   ragged tile, whose missing rows are padding positions).
+ *   Codes are offset-binary: u = q + 2^(b-1) for b >= 2, u = (q+1)/2 for b = 1.
+ *
+ *   Sections (each starts at a 256-byte aligned offset from the blob start):
+ *   [0] unit table  uint32[n_units+1][8]: row u = {e0,e1,e2,e3, wmap_word, 0,0,0}
+ *                   e_c = index of unit u's first class-c entry in section c;
+ *                   wmap_word = index of unit u's first 64-bit word in [1].
+ *                   Row n_units holds the totals.
+ *   [1] wmap        uint64 words.  Unit u owns 2*W_u words, W_u = ceil(C_k*R/64):
+ *                   W_u words of plane 0 (class bit 0) then W_u of plane 1
+ *                   (class bit 1); position p is bit p%64 of word p/64.
+ *                   Padding positions and the tail of the last word are 0.
+ *   [2+c] codes[c]  class-c entries (groups of width 2^c), ordered by unit,
+ *                   then by position p.  An entry is 8*b bytes = 2b little-
+ *                   endian uint32 words.  Weight pair i (weights 2i, 2i+1 of
+ *                   the group, i = 0..31) lives in word i / (16/b), field
+ *                   f = i % (16/b): the code of weight 2i in bits
+ *                   [f*b, f*b+b) and the code of weight 2i+1 in bits
+ *                   [16+f*b, 16+f*b+b).
+ *   [6+c] scales[c] IEEE fp16 bit patterns (uint16), one per class-c entry,
+ *                   same order as codes[c].
+ *
+ * Conventions for every call:
+ *   - The caller owns every buffer.  No entry point allocates device memory or
+ *     keeps global state; calls on different streams are independent.
+ *   - vbq_pack* run synchronously on the host.  Device entry points enqueue
+ *     work on the given stream and return; errors detected before the launch
+ *     are returned, a failed launch returns VBQ_ERR_HIP.
+ *   - Device pointers must be 16-byte aligned; x / X are contiguous fp16.
+ *   - Nothing throws across this interface.
+ */
+#ifndef VBQ_H
+#define VBQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum vbq_status {
+  VBQ_OK = 0,
+  VBQ_ERR_NULL = 1,        /* a required pointer is NULL                      */
+  VBQ_ERR_SHAPE = 2,       /* N < 1, K < 64, K % 64 != 0, M out of range, ... */
+  VBQ_ERR_BITS = 3,        /* a bit-width outside {1,2,4,8}                   */
+  VBQ_ERR_CODE_RANGE = 4,  /* a code outside its width's level set            */
+  VBQ_ERR_NONFINITE = 5,   /* NaN or Inf in weights, or a non-finite scale    */
+  VBQ_ERR_SCALE_RANGE = 6, /* a scale that rounds to Inf in fp16, or < 0      */
+  VBQ_ERR_BUFFER = 7,      /* buffer too small or misaligned                  */
+  VBQ_ERR_DESC = 8,        /* descriptor magic / version / shape mismatch     */
+  VBQ_ERR_HIP = 9,         /* the HIP runtime reported an error               */
+  VBQ_ERR_UNSUPPORTED = 10 /* option outside the supported range              */
+} vbq_status;
+
+#define VBQ_MAGIC 0x31514256u /* "VBQ1" little-endian */
+#define VBQ_LAYOUT_VERSION 1u
+#define VBQ_GROUP 64
+#define VBQ_NSECTIONS 10
+#define VBQ_MAX_M 16
+
+/* Section indices in vbq_desc.section_off / section_len. */
+enum { VBQ_SEC_UNITS = 0, VBQ_SEC_WMAP = 1, VBQ_SEC_CODES0 = 2, VBQ_SEC_SCALES0 = 6 };
+
+/* Host-side description of one packed matrix (plain old data). */
+typedef struct vbq_desc {
+  uint32_t magic;        /* VBQ_MAGIC                                  */
+  uint32_t version;      /* VBQ_LAYOUT_VERSION                         */
+  int64_t N, K;          /* rows (outputs) and columns (inputs)        */
+  int32_t group;         /* always 64                                  */
+  int32_t tile_rows;     /* R                                          */
+  int32_t chunk_groups;  /* C                                          */
+  int32_t reserved0;
+  int64_t n_tiles, n_chunks, n_units;
+  int64_t n_entries[4];  /* number of groups of width 1,2,4,8          */
+  uint64_t section_off[VBQ_NSECTIONS];
+  uint64_t section_len[VBQ_NSECTIONS];
+  uint64_t total_bytes;  /* size of the blob                           */
+  uint32_t flags;        /* reserved, 0                                */
+  uint32_t reserved1;
+} vbq_desc;
+
+/* Packing options; a zero field selects the library's choice. */
+typedef struct vbq_pack_opts {
+  int32_t tile_rows;     /* 0 or a power of two in [16, 256]           */
+  int32_t chunk_groups;  /* 0 or 1..128 with tile_rows*chunk_groups <= 8192 */
+  uint32_t flags;        /* reserved, 0                                */
+  uint32_t n_threads;    /* host threads for packing; 0 = hardware     */
+} vbq_pack_opts;
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* vbq_status_string(vbq_status s);
+
+/* Layout version this library reads and writes. */
+uint32_t vbq_layout_version(void);
+
+/* Bytes of the blob that vbq_pack / vbq_pack_codes would write for a matrix
+ * with the given bit map.  bits: host uint8[N][K/64], each in {1,2,4,8}.
+ * opts may be NULL.  Also fills *desc_out (may be NULL) with the layout. */
+vbq_status vbq_pack_size(int64_t N, int64_t K, const uint8_t* bits,
+                         const vbq_pack_opts* opts, size_t* bytes,
+                         vbq_desc* desc_out);
+
+/* Quantize and pack (paper section 3.1, Eq. (1) and the 1-bit rule).
+ * W: host float32[N][K] row-major; bits: host uint8[N][K/64].
+ * blob: host buffer of blob_bytes >= vbq_pack_size() bytes, 8-byte aligned.
+ * On success fills *desc.  Errors: NULL, SHAPE, BITS, NONFINITE (NaN/Inf in
+ * W), SCALE_RANGE (a scale that overflows fp16), BUFFER, UNSUPPORTED. */
+vbq_status vbq_pack(int64_t N, int64_t K, const float* W, const uint8_t* bits,
+                    const vbq_pack_opts* opts, void* blob, size_t blob_bytes,
+                    vbq_desc* desc);
+
+/* Pack already-quantized codes.  q: host int8[N][K] (levels, not offset
+ * codes); scale_f16: host uint16[N][K/64] fp16 bit patterns; bits as above.
+ * Errors additionally: CODE_RANGE (q outside the width's level set),
+ * NONFINITE / SCALE_RANGE (scale is NaN/Inf or negative). */
+vbq_status vbq_pack_codes(int64_t N, int64_t K, const int8_t* q,
+                          const uint16_t* scale_f16, const uint8_t* bits,
+                          const vbq_pack_opts* opts, void* blob,
+                          size_t blob_bytes, vbq_desc* desc);
+
+/* Check a descriptor against this library's layout (magic, version, shape,
+ * section offsets inside total_bytes).  VBQ_OK or VBQ_ERR_DESC / NULL. */
+vbq_status vbq_desc_check(const vbq_desc* d);
+
+/* y[n] = sum_k w_hat[n][k] * x[k]   (fused dequantize + GEMV, paper section 6)
+ * blob_dev: the packed blob in device memory (desc->total_bytes bytes);
+ * x_dev: device fp16[K]; y_dev: device float32[N].  Asynchronous on stream
+ * (a hipStream_t; NULL = default stream).  The sum over each row is taken in
+ * a fixed order, so results are bitwise reproducible for a given blob. */
+vbq_status vbq_gemv(const vbq_desc* desc, const void* blob_dev,
+                    const void* x_dev, float* y_dev, void* stream);
+
+/* Y[m][n] = sum_k w_hat[n][k] * X[m][k] for m < M, 0 <= M <= 16
+ * (small-batch decode).  X_dev: device fp16 rows with stride ldx >= K
+ * elements (ldx % 8 == 0); Y_dev: device float32 rows with stride ldy >= N.
+ * M == 0 is a no-op.  Weights are streamed once for all M rows. */
+vbq_status vbq_gemm_small(const vbq_desc* desc, const void* blob_dev,
+                          int64_t M, const void* X_dev, int64_t ldx,
+                          float* Y_dev, int64_t ldy, void* stream);
+
+/* W_dev[n][k] = w_hat[n][k] = s*q as float32 (exact), device float32[N][K].
+ * For checking the packed stream against the quantizer bit for bit. */
+vbq_status vbq_dequant(const vbq_desc* desc, const void* blob_dev,
+                       float* W_dev, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VBQ_H */
