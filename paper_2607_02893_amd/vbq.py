@@ -1,0 +1,234 @@
+"""ctypes binding of libvbq (C ABI declared in include/vbq.h).
+
+Argument marshalling only: every step of the path -- quantizing and packing on
+the host, decoding and multiplying on the GPU -- runs inside libvbq.  PyTorch
+is used for device memory and streams.  If libvbq.so has not been built this
+module raises on import; there is no fallback.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libvbq.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_02893_amd.build` "
+                      "(or __graft_entry__.build()); there is no fallback path")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+MAGIC = 0x31514256
+LAYOUT_VERSION = 1
+NSECTIONS = 10
+MAX_M = 16
+STATUS = {0: "VBQ_OK", 1: "VBQ_ERR_NULL", 2: "VBQ_ERR_SHAPE", 3: "VBQ_ERR_BITS", 4: "VBQ_ERR_CODE_RANGE",
+          5: "VBQ_ERR_NONFINITE", 6: "VBQ_ERR_SCALE_RANGE", 7: "VBQ_ERR_BUFFER", 8: "VBQ_ERR_DESC",
+          9: "VBQ_ERR_HIP", 10: "VBQ_ERR_UNSUPPORTED"}
+# exported symbols, in the order include/vbq.h declares them
+EXPORTS = ("vbq_status_string", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
+           "vbq_desc_check", "vbq_gemv", "vbq_gemm_small", "vbq_dequant")
+
+
+class VbqDesc(ctypes.Structure):
+    _fields_ = [("magic", ctypes.c_uint32), ("version", ctypes.c_uint32),
+                ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("group", ctypes.c_int32), ("tile_rows", ctypes.c_int32),
+                ("chunk_groups", ctypes.c_int32), ("reserved0", ctypes.c_int32),
+                ("n_tiles", ctypes.c_int64), ("n_chunks", ctypes.c_int64), ("n_units", ctypes.c_int64),
+                ("n_entries", ctypes.c_int64 * 4),
+                ("section_off", ctypes.c_uint64 * NSECTIONS), ("section_len", ctypes.c_uint64 * NSECTIONS),
+                ("total_bytes", ctypes.c_uint64), ("flags", ctypes.c_uint32), ("reserved1", ctypes.c_uint32)]
+
+    def info(self):
+        """Plain-dict view (same keys as the oracle's pack info)."""
+        return {"N": self.N, "K": self.K, "R": self.tile_rows, "C": self.chunk_groups,
+                "T": self.n_tiles, "U": self.n_chunks, "units": self.n_units,
+                "n_entries": list(self.n_entries), "section_off": list(self.section_off),
+                "section_len": list(self.section_len), "total_bytes": self.total_bytes}
+
+
+class VbqPackOpts(ctypes.Structure):
+    _fields_ = [("tile_rows", ctypes.c_int32), ("chunk_groups", ctypes.c_int32),
+                ("flags", ctypes.c_uint32), ("n_threads", ctypes.c_uint32)]
+
+
+_P = ctypes.c_void_p
+_lib.vbq_status_string.restype = ctypes.c_char_p
+_lib.vbq_status_string.argtypes = [ctypes.c_int]
+_lib.vbq_layout_version.restype = ctypes.c_uint32
+_lib.vbq_layout_version.argtypes = []
+_lib.vbq_pack_size.restype = ctypes.c_int
+_lib.vbq_pack_size.argtypes = [ctypes.c_int64, ctypes.c_int64, _P, ctypes.POINTER(VbqPackOpts),
+                               ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(VbqDesc)]
+_lib.vbq_pack.restype = ctypes.c_int
+_lib.vbq_pack.argtypes = [ctypes.c_int64, ctypes.c_int64, _P, _P, ctypes.POINTER(VbqPackOpts), _P,
+                          ctypes.c_size_t, ctypes.POINTER(VbqDesc)]
+_lib.vbq_pack_codes.restype = ctypes.c_int
+_lib.vbq_pack_codes.argtypes = [ctypes.c_int64, ctypes.c_int64, _P, _P, _P, ctypes.POINTER(VbqPackOpts), _P,
+                                ctypes.c_size_t, ctypes.POINTER(VbqDesc)]
+_lib.vbq_desc_check.restype = ctypes.c_int
+_lib.vbq_desc_check.argtypes = [ctypes.POINTER(VbqDesc)]
+_lib.vbq_gemv.restype = ctypes.c_int
+_lib.vbq_gemv.argtypes = [ctypes.POINTER(VbqDesc), _P, _P, _P, _P]
+_lib.vbq_gemm_small.restype = ctypes.c_int
+_lib.vbq_gemm_small.argtypes = [ctypes.POINTER(VbqDesc), _P, ctypes.c_int64, _P, ctypes.c_int64, _P,
+                                ctypes.c_int64, _P]
+_lib.vbq_dequant.restype = ctypes.c_int
+_lib.vbq_dequant.argtypes = [ctypes.POINTER(VbqDesc), _P, _P, _P]
+
+
+class VbqError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        msg = _lib.vbq_status_string(status).decode()
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({msg})")
+
+
+def _check(status, where):
+    if status != 0:
+        raise VbqError(status, where)
+
+
+def status_string(status):
+    return _lib.vbq_status_string(status).decode()
+
+
+def layout_version():
+    return int(_lib.vbq_layout_version())
+
+
+def _opts(tile_rows=0, chunk_groups=0, n_threads=0):
+    return VbqPackOpts(tile_rows, chunk_groups, 0, n_threads)
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a is not None else None
+
+
+def pack_size(bits, K, tile_rows=0, chunk_groups=0):
+    bits = np.ascontiguousarray(bits, dtype=np.uint8)
+    nbytes = ctypes.c_size_t(0)
+    d = VbqDesc()
+    o = _opts(tile_rows, chunk_groups)
+    _check(_lib.vbq_pack_size(bits.shape[0], K, _ptr(bits), ctypes.byref(o), ctypes.byref(nbytes),
+                              ctypes.byref(d)), "vbq_pack_size")
+    return nbytes.value, d
+
+
+def _blob(nbytes):
+    # 256-byte aligned host buffer
+    raw = np.zeros(nbytes + 256, dtype=np.uint8)
+    off = (-raw.ctypes.data) % 256
+    return raw[off:off + nbytes]
+
+
+def pack(W, bits, tile_rows=0, chunk_groups=0, n_threads=0):
+    """Quantize float32 W[N][K] with bit map bits[N][K/64] and pack it (host)."""
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    bits = np.ascontiguousarray(bits, dtype=np.uint8)
+    N, K = W.shape
+    nbytes, _ = pack_size(bits, K, tile_rows, chunk_groups)
+    blob = _blob(nbytes)
+    d = VbqDesc()
+    o = _opts(tile_rows, chunk_groups, n_threads)
+    _check(_lib.vbq_pack(N, K, _ptr(W), _ptr(bits), ctypes.byref(o), _ptr(blob), nbytes, ctypes.byref(d)),
+           "vbq_pack")
+    return blob, d
+
+
+def pack_codes(q, scales, bits, tile_rows=0, chunk_groups=0, n_threads=0):
+    """Pack levels q int8[N][K], fp16 scale bits uint16[N][K/64] and bits uint8[N][K/64] (host)."""
+    q = np.ascontiguousarray(q, dtype=np.int8)
+    scales = np.ascontiguousarray(scales, dtype=np.uint16)
+    bits = np.ascontiguousarray(bits, dtype=np.uint8)
+    N, K = q.shape
+    nbytes, _ = pack_size(bits, K, tile_rows, chunk_groups)
+    blob = _blob(nbytes)
+    d = VbqDesc()
+    o = _opts(tile_rows, chunk_groups, n_threads)
+    _check(_lib.vbq_pack_codes(N, K, _ptr(q), _ptr(scales), _ptr(bits), ctypes.byref(o), _ptr(blob), nbytes,
+                               ctypes.byref(d)), "vbq_pack_codes")
+    return blob, d
+
+
+def desc_check(d):
+    return _lib.vbq_desc_check(ctypes.byref(d))
+
+
+# ------------------------------------------------------------------ device side
+
+def _stream_handle(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class PackedMatrix:
+    """A packed matrix resident in device memory (torch uint8 tensor) plus its descriptor."""
+
+    def __init__(self, blob, desc, device="cuda"):
+        import torch
+        self.desc = desc
+        self.N, self.K = desc.N, desc.K
+        t = torch.from_numpy(np.asarray(blob, dtype=np.uint8))
+        # torch's caching allocator returns 256-byte aligned blocks
+        self.blob = t.to(device)
+        if self.blob.data_ptr() % 256:
+            raise VbqError(7, "PackedMatrix")
+
+    @property
+    def nbytes(self):
+        return int(self.desc.total_bytes)
+
+    def gemv(self, x, y=None, stream=None):
+        """y[N] (float32) = w_hat @ x, x a contiguous fp16 device tensor of length K."""
+        import torch
+        if x.dtype != torch.float16 or not x.is_contiguous() or x.numel() != self.K:
+            raise ValueError("x must be a contiguous float16 tensor of length K")
+        if y is None:
+            y = torch.empty(self.N, dtype=torch.float32, device=x.device)
+        _check(_lib.vbq_gemv(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()),
+                             ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()),
+                             _stream_handle(stream)), "vbq_gemv")
+        return y
+
+    def gemm_small(self, X, Y=None, stream=None):
+        """Y[M][N] (float32) = X @ w_hat^T for an fp16 device tensor X[M][K], M <= 16."""
+        import torch
+        if X.dtype != torch.float16 or X.dim() != 2 or X.shape[1] != self.K or X.stride(1) != 1:
+            raise ValueError("X must be a float16 [M, K] tensor with unit column stride")
+        M = X.shape[0]
+        if Y is None:
+            Y = torch.empty((M, self.N), dtype=torch.float32, device=X.device)
+        _check(_lib.vbq_gemm_small(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()), M,
+                                   ctypes.c_void_p(X.data_ptr()), X.stride(0), ctypes.c_void_p(Y.data_ptr()),
+                                   Y.stride(0), _stream_handle(stream)), "vbq_gemm_small")
+        return Y
+
+    def dequant(self, W=None, stream=None):
+        """w_hat as a float32 [N, K] device tensor (exact)."""
+        import torch
+        if W is None:
+            W = torch.empty((self.N, self.K), dtype=torch.float32, device=self.blob.device)
+        _check(_lib.vbq_dequant(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()),
+                                ctypes.c_void_p(W.data_ptr()), _stream_handle(stream)), "vbq_dequant")
+        return W
+
+
+def raw_gemv(desc, blob_ptr, x_ptr, y_ptr, stream_ptr):
+    """vbq_gemv on raw device addresses (no checks beyond the library's own)."""
+    return _lib.vbq_gemv(ctypes.byref(desc), ctypes.c_void_p(blob_ptr), ctypes.c_void_p(x_ptr),
+                         ctypes.c_void_p(y_ptr), ctypes.c_void_p(stream_ptr))
+
+
+def raw_gemm_small(desc, blob_ptr, M, X_ptr, ldx, Y_ptr, ldy, stream_ptr):
+    return _lib.vbq_gemm_small(ctypes.byref(desc), ctypes.c_void_p(blob_ptr), M, ctypes.c_void_p(X_ptr), ldx,
+                               ctypes.c_void_p(Y_ptr), ldy, ctypes.c_void_p(stream_ptr))
+
+
+def lib():
+    """The loaded ctypes library (for symbol checks)."""
+    return _lib

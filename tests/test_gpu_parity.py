@@ -1,0 +1,204 @@
+"""GPU parity: the HIP path (through the C ABI) against the double-precision oracle.
+
+Bars:
+  * dequantized weights: bit-exact (s*q is exact in float32);
+  * one-hot probe x = e_k through vbq_gemv: column k of w_hat, bit-exact;
+  * outputs: tests/parity.py rule, tol 2e-3 (fp32 accumulation);
+  * repeated calls: bitwise identical (fixed summation order).
+Inputs come from paper_2607_02893_amd.synth (seeded); expected values come
+from oracle/ only.
+"""
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import layout as olayout  # noqa: E402
+from oracle import matmul as omatmul  # noqa: E402
+from oracle import quant as oquant  # noqa: E402
+from paper_2607_02893_amd import synth  # noqa: E402
+from tests import parity  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def vbq():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    from paper_2607_02893_amd import vbq as v
+    return v
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _packed(vbq, q, s, bits, R=0, C=0):
+    blob, d = vbq.pack_codes(q, s, bits, tile_rows=R, chunk_groups=C)
+    return vbq.PackedMatrix(blob, d)
+
+
+def _x_dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+GEOMS = [(512, 512, 0, 0), (1, 64, 16, 1), (37, 320, 16, 2), (100, 768, 64, 12), (130, 1024, 32, 5),
+         (300, 640, 256, 3), (17, 896, 16, 7), (1000, 4096, 64, 64), (96, 14336, 16, 112)]
+
+
+@pytest.mark.parametrize("N,K,R,C", GEOMS)
+def test_dequant_bit_exact(vbq, N, K, R, C):
+    _say(f"dequant N={N} K={K} R={R} C={C}")
+    bits, q, s = synth.make_matrix(synth.MatrixSpec("t", N, K, N, K), 41)
+    Wp = _packed(vbq, q, s, bits, R, C)
+    W = Wp.dequant().cpu().numpy()
+    want = omatmul.dequant(q, s)
+    assert np.array_equal(W.astype(np.float64), want)
+
+
+@pytest.mark.parametrize("N,K,R,C", GEOMS)
+def test_gemv_matches_oracle(vbq, N, K, R, C):
+    _say(f"gemv N={N} K={K} R={R} C={C}")
+    spec = synth.MatrixSpec("t", N, K, N, K)
+    bits, q, s = synth.make_matrix(spec, 43)
+    x = synth.make_x(spec, 43)[0]
+    Wp = _packed(vbq, q, s, bits, R, C)
+    y = Wp.gemv(_x_dev(x)).cpu().numpy()
+    rel = parity.check(y, omatmul.gemv(q, s, x), omatmul.row_magnitude(q, s, x), what=f"gemv {N}x{K}")
+    _say(f"  max rel err {rel:.2e}")
+
+
+def test_one_hot_probe_is_exact(vbq):
+    spec = synth.MatrixSpec("t", 0, 0, 300, 1024)
+    bits, q, s = synth.make_matrix(spec, 47)
+    Wp = _packed(vbq, q, s, bits, 32, 5)
+    W = omatmul.dequant(q, s)
+    for k in (0, 1, 62, 63, 64, 333, 1023):
+        e = np.zeros(1024, dtype=np.float16)
+        e[k] = 1.0
+        y = Wp.gemv(_x_dev(e)).cpu().numpy()
+        assert np.array_equal(y.astype(np.float64), W[:, k]), k
+        e[k] = -2.0
+        y = Wp.gemv(_x_dev(e)).cpu().numpy()
+        assert np.array_equal(y.astype(np.float64), -2.0 * W[:, k]), k
+
+
+def test_gemv_bitwise_repeatable(vbq):
+    spec = synth.MatrixSpec("t", 0, 0, 2048, 4096)
+    bits, q, s = synth.make_matrix(spec, 53)
+    Wp = _packed(vbq, q, s, bits)
+    x = _x_dev(synth.make_x(spec, 53)[0])
+    y0 = Wp.gemv(x).cpu().numpy()
+    for _ in range(3):
+        assert np.array_equal(Wp.gemv(x).cpu().numpy(), y0)
+
+
+@pytest.mark.parametrize("bits_u", [1, 2, 4, 8])
+def test_uniform_width_vs_dense_float32(vbq, bits_u):
+    """Uniform-width matrices against a plain PyTorch float32 dense product of
+    the dequantized weights, and the oracle."""
+    spec = synth.MatrixSpec("u", 0, bits_u, 768, 2048, uniform_bits=bits_u)
+    bits, q, s = synth.make_matrix(spec, 59)
+    x = synth.make_x(spec, 59)[0]
+    Wp = _packed(vbq, q, s, bits)
+    xd = _x_dev(x)
+    y = Wp.gemv(xd)
+    dense = torch.from_numpy(omatmul.dequant(q, s).astype(np.float32)).cuda()
+    yref32 = (dense @ xd.float()).cpu().numpy()
+    ystar = omatmul.gemv(q, s, x)
+    rm = omatmul.row_magnitude(q, s, x)
+    parity.check(y.cpu().numpy(), ystar, rm, what=f"uniform {bits_u}")
+    parity.check(yref32, ystar, rm, what="torch fp32 dense")
+
+
+@pytest.mark.parametrize("M", [1, 2, 3, 4, 8, 11, 16])
+@pytest.mark.parametrize("N,K,R,C", [(257, 768, 16, 12), (130, 4096, 64, 64), (64, 14336, 16, 112)])
+def test_gemm_small_matches_oracle(vbq, M, N, K, R, C):
+    _say(f"gemm_small M={M} N={N} K={K}")
+    spec = synth.MatrixSpec("t", 1, 2, N, K)
+    bits, q, s = synth.make_matrix(spec, 61)
+    X = synth.make_x(spec, 61, M=M)
+    Wp = _packed(vbq, q, s, bits, R, C)
+    Y = Wp.gemm_small(_x_dev(X)).cpu().numpy()
+    Ystar = omatmul.gemm(q, s, X)
+    for m in range(M):
+        parity.check(Y[m], Ystar[m], omatmul.row_magnitude(q, s, X[m]), what=f"gemm m={m}")
+
+
+def test_gemm_small_strided_and_empty(vbq):
+    spec = synth.MatrixSpec("t", 1, 3, 200, 512)
+    bits, q, s = synth.make_matrix(spec, 67)
+    X = synth.make_x(spec, 67, M=5)
+    Wp = _packed(vbq, q, s, bits)
+    Xpad = torch.zeros((5, 512 + 64), dtype=torch.float16, device="cuda")
+    Xpad[:, :512] = _x_dev(X)
+    Ypad = torch.full((5, 256), 7.0, dtype=torch.float32, device="cuda")
+    Wp.gemm_small(Xpad[:, :512], Ypad[:, :200])
+    Yh = Ypad.cpu().numpy()
+    Ystar = omatmul.gemm(q, s, X)
+    for m in range(5):
+        parity.check(Yh[m, :200], Ystar[m], omatmul.row_magnitude(q, s, X[m]))
+    assert np.all(Yh[:, 200:] == 7.0)  # nothing written past N
+    Wp.gemm_small(Xpad[:0, :512], Ypad[:0, :200])  # M = 0 is a no-op
+
+
+def test_quantizer_path_bit_exact(vbq):
+    """vbq_pack (C++ quantizer) -> device dequant equals oracle quantize -> dequant."""
+    rng = synth.rng_for(71)
+    W = synth.draw_weights(rng, 333, 1024, std=0.05)
+    bits = synth.draw_bits(rng, 333, 16, synth.MIX_PILOT)
+    blob, d = vbq.pack(W, bits)
+    Wp = vbq.PackedMatrix(blob, d)
+    q, s = oquant.quantize(W, bits)
+    assert np.array_equal(Wp.dequant().cpu().numpy().astype(np.float64), omatmul.dequant(q, s))
+
+
+def test_blob_roundtrip_through_device(vbq):
+    spec = synth.MatrixSpec("t", 2, 2, 77, 640)
+    bits, q, s = synth.make_matrix(spec, 73)
+    Wp = _packed(vbq, q, s, bits, 16, 3)
+    back = Wp.blob.cpu().numpy()
+    q2, s2, b2 = olayout.unpack(back, Wp.desc.info())
+    assert np.array_equal(q2, q) and np.array_equal(s2, s) and np.array_equal(b2, bits)
+
+
+# ------------------------------------------------------------------ full-size workloads (sampled rows)
+
+def _sampled_check(vbq, spec, seed, M=1, n_rows=192):
+    bits, q, s = synth.make_matrix(spec, seed)
+    X = synth.make_x(spec, seed, M=M)
+    Wp = _packed(vbq, q, s, bits)
+    if M == 1:
+        Y = Wp.gemv(_x_dev(X[0])).cpu().numpy()[None, :]
+    else:
+        Y = Wp.gemm_small(_x_dev(X)).cpu().numpy()
+    rows = np.unique(np.concatenate([np.arange(min(16, spec.N)), np.arange(max(0, spec.N - 16), spec.N),
+                                     synth.rng_for(seed, 9).choice(spec.N, size=min(n_rows, spec.N), replace=False)]))
+    worst = 0.0
+    for m in range(M):
+        ystar = omatmul.gemv(q[rows], s[rows], X[m])
+        worst = max(worst, parity.check(Y[m, rows], ystar, omatmul.row_magnitude(q[rows], s[rows], X[m]),
+                                        what=f"{spec.name} L{spec.layer} m={m}"))
+    assert np.all(np.isfinite(Y))
+    return worst
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_workload_matrices_full_size(vbq, cfg):
+    wl = synth.workload(cfg)
+    mats = wl.matrices if cfg == 0 else [m for m in wl.matrices if m.layer in (0, 1) and m.proj in (0, 3)] + \
+        [m for m in wl.matrices if m.layer == 0 and m.proj in (1, 2)] + [wl.matrices[-1]]
+    for spec in mats:
+        for M in ((1, 16) if cfg == 4 else (1,)):
+            w = _sampled_check(vbq, spec, wl.seed, M=M)
+            _say(f"cfg{cfg} {spec.name} L{spec.layer} {spec.N}x{spec.K} M={M}: max rel err {w:.2e}")
+
+
+@pytest.mark.parametrize("ub", [1, 2, 4, 8])
+def test_workload4_uniform_variants(vbq, ub):
+    wl = synth.workload(4, uniform_bits=ub)
+    for spec in (wl.matrices[2], wl.matrices[-1]):
+        w = _sampled_check(vbq, spec, wl.seed)
+        _say(f"cfg4 u{ub} {spec.name} {spec.N}x{spec.K}: max rel err {w:.2e}")

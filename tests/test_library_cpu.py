@@ -1,0 +1,200 @@
+"""Host-side checks of libvbq that need no GPU.
+
+* the library loads and exports every entry point include/vbq.h declares;
+* vbq_pack_codes writes exactly the bytes of the oracle's independent packer
+  (bit-exact, several geometries, ragged tiles and chunks);
+* vbq_pack (C++ quantizer) matches the oracle quantizer + packer byte for byte,
+  including rounding ties, stored-scale rounding, sign(0), zero groups and
+  subnormal scales;
+* every documented error path returns its status code.
+"""
+
+import ctypes
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import layout as olayout
+from oracle import quant as oquant
+from paper_2607_02893_amd import synth
+from paper_2607_02893_amd import vbq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_exports_every_declared_symbol():
+    with open(os.path.join(ROOT, "include", "vbq.h")) as f:
+        hdr = f.read()
+    declared = set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\*?\s+\*?(vbq_[a-z_0-9]+)\s*\(", hdr, re.M))
+    assert declared == set(vbq.EXPORTS), declared ^ set(vbq.EXPORTS)
+    lib = vbq.lib()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert vbq.layout_version() == vbq.LAYOUT_VERSION == 1
+    assert ctypes.sizeof(vbq.VbqDesc) == 272
+    for s in range(11):
+        assert vbq.status_string(s)
+
+
+def _random_codes(rng, N, K, mix=synth.MIX_PILOT):
+    bits = synth.draw_bits(rng, N, K // 64, mix)
+    return bits, synth.draw_levels(rng, bits), synth.draw_scales(rng, N, K // 64)
+
+
+@pytest.mark.parametrize("N,K,R,C", [(1, 64, 16, 1), (37, 320, 16, 2), (100, 768, 64, 12), (130, 1024, 32, 5),
+                                     (64, 4096, 64, 64), (300, 640, 256, 3), (513, 512, 0, 0), (17, 896, 16, 7)])
+def test_pack_codes_bytes_match_oracle(N, K, R, C):
+    rng = synth.rng_for(5, N, K)
+    bits, q, s = _random_codes(rng, N, K)
+    blob, d = vbq.pack_codes(q, s, bits, tile_rows=R, chunk_groups=C)
+    assert vbq.desc_check(d) == 0
+    info = d.info()
+    oblob, oinfo = olayout.pack(q, s, bits, info["R"], info["C"])
+    for key in ("T", "U", "units", "n_entries", "section_off", "section_len", "total_bytes"):
+        assert info[key] == oinfo[key], key
+    assert np.array_equal(np.asarray(blob), oblob)
+
+
+def test_pack_codes_hand_fixture(golden_dir):
+    with open(os.path.join(golden_dir, "layout_tiny.json")) as f:
+        fx = json.load(f)
+    N, K = fx["N"], fx["K"]
+    q = np.zeros((N, K), dtype=np.int8)
+    s = np.zeros((N, K // 64), dtype=np.uint16)
+    for r in range(N):
+        for j in range(K // 64):
+            g = fx["groups"][f"r{r}j{j}"]
+            qq = [g["default_q"]] * 64
+            for k, v in g["q_overrides"].items():
+                qq[int(k)] = v
+            q[r, 64 * j:64 * j + 64] = qq
+            s[r, j] = int(g["s_bits"], 16)
+    blob, d = vbq.pack_codes(q, s, np.array(fx["bits"], dtype=np.uint8), tile_rows=fx["R"], chunk_groups=fx["C"])
+    ex = fx["expected"]
+    assert list(d.section_off) == ex["section_off"] and list(d.section_len) == ex["section_len"]
+    assert d.total_bytes == ex["total_bytes"]
+    b = np.asarray(blob)
+    wmap = np.frombuffer(b[256:272].tobytes(), dtype=np.uint64)
+    assert [int(w) for w in wmap] == [int(w, 16) for w in ex["wmap"]]
+    codes8 = np.frombuffer(b[1024:1088].tobytes(), dtype=np.uint32)
+    assert [int(w) for w in codes8] == [int(w, 16) for w in fx["groups"]["r1j0"]["words"]]
+
+
+def _quant_inputs(rng, N, K):
+    W = synth.draw_weights(rng, N, K, std=1.0)
+    bits = synth.draw_bits(rng, N, K // 64, {1: .25, 2: .25, 4: .25, 8: .25})
+    W = W * rng.uniform(1e-3, 10, (N, 1)).astype(np.float32)
+    # special groups: zeros, ties, negative zero, tiny (subnormal scales), large
+    W[0, :64] = 0.0
+    W[1, :64] = np.array([7, -3.5, 0.5, -0.49, 2.5, 1.5, -7, 0] * 8, dtype=np.float32)
+    bits[1, 0] = 4
+    W[2, :64] = -0.0
+    bits[2, 0] = 1
+    W[3, :64] = rng.standard_normal(64).astype(np.float32) * 1e-6
+    W[4, :64] = rng.standard_normal(64).astype(np.float32) * 3000
+    W[5, 64:128] = np.array([0.3, -0.2, 0.15002, -0.1] * 16, dtype=np.float32)
+    bits[5, 1] = 2
+    return W, bits
+
+
+@pytest.mark.parametrize("N,K,R,C", [(40, 512, 16, 0), (97, 768, 32, 5), (8, 128, 16, 1)])
+def test_pack_quantizer_matches_oracle(N, K, R, C):
+    rng = synth.rng_for(9, N, K)
+    W, bits = _quant_inputs(rng, N, K)
+    blob, d = vbq.pack(W, bits, tile_rows=R, chunk_groups=C)
+    q, s = oquant.quantize(W, bits)
+    oblob, _ = olayout.pack(q, s, bits, d.tile_rows, d.chunk_groups)
+    assert np.array_equal(np.asarray(blob), oblob)
+    q2, s2, b2 = olayout.unpack(np.asarray(blob), d.info())
+    assert np.array_equal(q2, q) and np.array_equal(s2, s) and np.array_equal(b2, bits)
+
+
+def test_auto_geometry_is_valid():
+    for N, K in [(512, 512), (768, 3072), (4096, 14336), (28672, 4096), (128256, 4096), (1, 64)]:
+        nbytes, d = vbq.pack_size(np.ones((N, K // 64), dtype=np.uint8), K)
+        assert vbq.desc_check(d) == 0 and nbytes == d.total_bytes
+        assert d.tile_rows in (16, 32, 64) and 1 <= d.chunk_groups <= 128
+        assert d.tile_rows * d.chunk_groups <= 8192
+
+
+# ------------------------------------------------------------------ error paths
+
+def _status(fn):
+    with pytest.raises(vbq.VbqError) as ei:
+        fn()
+    return vbq.STATUS[ei.value.status]
+
+
+def test_error_paths():
+    rng = synth.rng_for(3)
+    bits, q, s = _random_codes(rng, 8, 256)
+    assert _status(lambda: vbq.pack_codes(q[:, :200], s, bits)) in ("VBQ_ERR_SHAPE", "VBQ_ERR_BITS")
+    bad = bits.copy()
+    bad[3, 2] = 3
+    assert _status(lambda: vbq.pack_codes(q, s, bad)) == "VBQ_ERR_BITS"
+    qq = q.copy()
+    bits2 = bits.copy()
+    bits2[0, 0] = 2
+    qq[0, :64] = 0
+    qq[0, 5] = -2  # the code for -2^(b-1) is outside the level set
+    assert _status(lambda: vbq.pack_codes(qq, s, bits2)) == "VBQ_ERR_CODE_RANGE"
+    bits1 = bits.copy()
+    bits1[0, 0] = 1
+    qq[0, :64] = 1
+    qq[0, 7] = 0  # 1-bit levels are +-1 only
+    assert _status(lambda: vbq.pack_codes(qq, s, bits1)) == "VBQ_ERR_CODE_RANGE"
+    ss = s.copy()
+    ss[1, 1] = 0x7C00  # +inf
+    assert _status(lambda: vbq.pack_codes(q, ss, bits)) == "VBQ_ERR_NONFINITE"
+    ss[1, 1] = 0xBC00  # -1.0
+    assert _status(lambda: vbq.pack_codes(q, ss, bits)) == "VBQ_ERR_SCALE_RANGE"
+    W = np.zeros((4, 128), dtype=np.float32)
+    b4 = np.full((4, 2), 2, dtype=np.uint8)
+    W[1, 3] = np.nan
+    assert _status(lambda: vbq.pack(W, b4)) == "VBQ_ERR_NONFINITE"
+    W[1, 3] = np.inf
+    assert _status(lambda: vbq.pack(W, b4)) == "VBQ_ERR_NONFINITE"
+    W[1, 3] = 1e6  # max|w|/1 overflows fp16
+    assert _status(lambda: vbq.pack(W, b4)) == "VBQ_ERR_SCALE_RANGE"
+    W[1, 3] = 0.0
+    assert _status(lambda: vbq.pack(W, b4, tile_rows=24)) == "VBQ_ERR_UNSUPPORTED"
+    assert _status(lambda: vbq.pack(W, b4, tile_rows=64, chunk_groups=200)) == "VBQ_ERR_UNSUPPORTED"
+    assert _status(lambda: vbq.pack_size(np.ones((4, 2), np.uint8), 100)) == "VBQ_ERR_SHAPE"
+    assert _status(lambda: vbq.pack_size(np.ones((4, 0), np.uint8), 0)) == "VBQ_ERR_SHAPE"
+
+
+def test_null_and_buffer_errors():
+    lib = vbq.lib()
+    bits = np.ones((2, 2), dtype=np.uint8)
+    nbytes = ctypes.c_size_t(0)
+    assert lib.vbq_pack_size(2, 128, None, None, ctypes.byref(nbytes), None) == 1
+    q = np.ones((2, 128), dtype=np.int8)
+    s = np.full((2, 2), 0x3C00, dtype=np.uint16)
+    d = vbq.VbqDesc()
+    assert lib.vbq_pack_size(2, 128, bits.ctypes.data_as(ctypes.c_void_p), None, ctypes.byref(nbytes), None) == 0
+    small = np.zeros((int(nbytes.value) - 256) // 8, dtype=np.uint64)
+    assert lib.vbq_pack_codes(2, 128, q.ctypes.data_as(ctypes.c_void_p), s.ctypes.data_as(ctypes.c_void_p),
+                              bits.ctypes.data_as(ctypes.c_void_p), None, small.ctypes.data_as(ctypes.c_void_p),
+                              small.nbytes, ctypes.byref(d)) == 7
+    assert lib.vbq_pack_codes(2, 128, None, s.ctypes.data_as(ctypes.c_void_p), bits.ctypes.data_as(ctypes.c_void_p),
+                              None, small.ctypes.data_as(ctypes.c_void_p), small.nbytes, ctypes.byref(d)) == 1
+    # device entry points reject bad descriptors before touching the GPU
+    assert lib.vbq_gemv(None, None, None, None, None) == 1
+    bad = vbq.VbqDesc()
+    assert lib.vbq_gemv(ctypes.byref(bad), ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256),
+                        None) == 8
+    _, good = vbq.pack_codes(q, s, bits)
+    assert vbq.desc_check(good) == 0
+    good.version = 2
+    assert vbq.desc_check(good) == 8
+    good.version = 1
+    good.section_len[3] += 1
+    assert vbq.desc_check(good) == 8
+    good.section_len[3] -= 1
+    assert lib.vbq_gemm_small(ctypes.byref(good), ctypes.c_void_p(256), 17, None, 128, None, 2, None) == 2
+    assert lib.vbq_gemm_small(ctypes.byref(good), ctypes.c_void_p(256), 0, None, 128, None, 2, None) == 0
+    assert lib.vbq_gemv(ctypes.byref(good), ctypes.c_void_p(100), ctypes.c_void_p(256), ctypes.c_void_p(256),
+                        None) == 7
