@@ -1,0 +1,309 @@
+"""Decode-step benchmark of the fused dequant-GEMV over packed VBQ weights.
+
+A step is every linear GEMV of one decode token of the chosen synthetic
+workload, in call order, on one stream (Q|K|V and gate|up are stored as one
+row-concatenated matrix each, since they read the same input).  Inputs are
+resident in HBM before timing starts.  Default workload: the 9B-class step
+(d_model 4096, 32 layers, GQA K/V 1024, MLP 14336, vocab 128256, widths drawn
+from the {1:.69, 2:.15, 4:.12, 8:.04} mix), 129 GEMVs, ~1.95 GB streamed.
+
+    python bench.py [--steps K] [--warmup W] [--workload 0..4] [--gpus 1]
+
+Prints one JSON line.  `value` is effective GB/s = algorithmic bytes of the
+step / wall time per step (HIP-graph replay of the step).  The roofline block
+times every launch of the GEMV kernel with HIP events recorded on the stream
+it runs on.  cpu_baseline times the double-precision oracle on a bounded
+sample of the same workload (host cores; a baseline only).
+"""
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "fused dequant-GEMV effective HBM GB/s (% of peak) and µs per decode step"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(bits, N, K, M=1):
+    """Codes (8*b per group) + fp16 scales + 2-bit width map + x (fp16) + y (fp32)."""
+    groups = bits.size
+    codes = int(np.sum(8 * bits.astype(np.int64)))
+    wmap = groups / 4.0 if np.unique(bits).size > 1 else 0.0
+    return codes + 2 * groups + wmap + 2 * M * K + 4 * M * N
+
+
+def _gen_pack(task):
+    """Worker: draw one matrix and pack it with libvbq (host only)."""
+    idx, cfg, seed, spec = task
+    from paper_2607_02893_amd import synth, vbq
+    bits, q, s = synth.make_matrix(spec, seed)
+    blob, desc = vbq.pack_codes(q, s, bits, n_threads=1)
+    alg = algorithmic_bytes(bits, spec.N, spec.K)
+    return idx, np.asarray(blob).copy(), bytes(desc), alg, spec.N * spec.K
+
+
+def prepare(cfg, workers):
+    from paper_2607_02893_amd import synth
+    wl = synth.workload(cfg)
+    tasks = [(i, cfg, wl.seed, m) for i, m in enumerate(wl.matrices)]
+    out = [None] * len(tasks)
+    t0 = time.time()
+    if workers > 1:
+        import multiprocessing as mp
+        # fork before anything touches the GPU
+        with mp.get_context("fork").Pool(workers) as pool:
+            for r in pool.imap_unordered(_gen_pack, sorted(tasks, key=lambda t: -t[3].N * t[3].K)):
+                out[r[0]] = r
+    else:
+        for t in tasks:
+            r = _gen_pack(t)
+            out[r[0]] = r
+    log(f"generated + packed {len(tasks)} matrices in {time.time() - t0:.1f}s")
+    return wl, out
+
+
+def cpu_baseline(wl, budget_s=20.0):
+    """Oracle (numpy fp64 dequant + matvec) on the first matrices of the step
+    until the time budget is spent, scaled by weight count to a full step."""
+    from oracle import matmul as omatmul
+    from paper_2607_02893_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = None
+    total_w = sum(m.N * m.K for m in wl.matrices)
+    done_w, spent, names = 0, 0.0, []
+    for spec in wl.matrices:
+        bits, q, s = synth.make_matrix(spec, wl.seed)
+        x = synth.make_x(spec, wl.seed)[0]
+        t0 = time.perf_counter()
+        rows = max(1, (1 << 25) // spec.K)  # row blocks keep the fp64 matrix bounded
+        y = np.empty(spec.N)
+        for r0 in range(0, spec.N, rows):
+            y[r0:r0 + rows] = omatmul.gemv(q[r0:r0 + rows], s[r0:r0 + rows], x)
+        spent += time.perf_counter() - t0
+        done_w += spec.N * spec.K
+        names.append(f"{spec.name}{spec.layer}")
+        if spent >= budget_s:
+            break
+    s_per_step = spent * total_w / done_w
+    cores = len(os.sched_getaffinity(0))
+    return {"value": round(1e3 * s_per_step, 1), "unit": "ms/step", "cores": blas_threads or cores,
+            "host_cores_visible": cores, "kind": "oracle",
+            "sample": f"{len(names)} of {len(wl.matrices)} matrices ({done_w / 1e6:.0f}M of {total_w / 1e6:.0f}M "
+                      f"weights: {', '.join(names[:6])}{'...' if len(names) > 6 else ''}), "
+                      f"{spent:.1f}s, scaled by weight count",
+            "gb_per_s_equiv": None}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=3)
+    ap.add_argument("--workers", type=int, default=min(12, len(os.sched_getaffinity(0))))
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 (eager launches only)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the fused GEMV path has no multi-GPU mode in this build "
+              "(the row / K split that would shard it is described in the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    wl, packed = prepare(args.workload, args.workers)
+
+    import torch
+    from paper_2607_02893_amd import synth, vbq
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    mats = []
+    total_alg, total_w, blob_bytes = 0.0, 0, 0
+    for idx, blob, dbytes, alg, nw in packed:
+        desc = vbq.VbqDesc.from_buffer_copy(dbytes)
+        Wp = vbq.PackedMatrix(blob, desc, device=dev)
+        spec = wl.matrices[idx]
+        x = torch.from_numpy(np.ascontiguousarray(synth.make_x(spec, wl.seed)[0])).to(dev)
+        y = torch.empty(spec.N, dtype=torch.float32, device=dev)
+        mats.append((Wp, x, y, alg))
+        total_alg += alg
+        total_w += nw
+        blob_bytes += desc.total_bytes
+    del packed
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+
+    launch_args = [(m[0].desc, m[0].blob.data_ptr(), m[1].data_ptr(), m[2].data_ptr()) for m in mats]
+
+    def step():
+        for d, b, x, y in launch_args:
+            st = vbq.raw_gemv(d, b, x, y, sptr)
+            if st != 0:
+                raise vbq.VbqError(st, "vbq_gemv")
+
+    log(f"{len(mats)} GEMVs, {total_w / 1e9:.2f}G weights, algorithmic {total_alg / 1e6:.1f} MB/step, "
+        f"blobs {blob_bytes / 1e6:.1f} MB")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    if args.profile:
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        log(f"profile run: {args.steps} eager steps, {1e6 * dt:.1f} us/step")
+        print(json.dumps({"profile_run": True, "us_per_step_eager": round(1e6 * dt, 2)}), flush=True)
+        return
+
+    # eager timing
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    eager_s = (time.perf_counter() - t0) / args.steps
+    log(f"eager: {1e6 * eager_s:.1f} us/step")
+
+    # graph timing (same launches captured once, replayed)
+    graph_s = None
+    try:
+        g = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        with torch.cuda.stream(cap):
+            csp = cap.cuda_stream
+            g.capture_begin()
+            for d, b, x, y in launch_args:
+                st = vbq.raw_gemv(d, b, x, y, csp)
+                if st != 0:
+                    raise vbq.VbqError(st, "vbq_gemv (capture)")
+            g.capture_end()
+        stream.wait_stream(cap)
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        graph_s = (time.perf_counter() - t0) / args.steps
+        log(f"graph: {1e6 * graph_s:.1f} us/step")
+        # graph result equals eager result
+        ref = [m[2].clone() for m in mats[:3] + mats[-1:]]
+        step()
+        torch.cuda.synchronize()
+        for r, m in zip(ref, mats[:3] + mats[-1:]):
+            assert torch.equal(r, m[2]), "graph replay differs from eager launch"
+    except Exception as e:  # graph capture is an optimisation of the same launches
+        log(f"graph capture unavailable: {e}")
+
+    # per-launch kernel durations with events on the launch stream
+    n_ev = min(5, args.steps)
+    starts = [[torch.cuda.Event(enable_timing=True) for _ in mats] for _ in range(n_ev)]
+    ends = [[torch.cuda.Event(enable_timing=True) for _ in mats] for _ in range(n_ev)]
+    for r in range(n_ev):
+        for i, (d, b, x, y) in enumerate(launch_args):
+            starts[r][i].record(stream)
+            vbq.raw_gemv(d, b, x, y, sptr)
+            ends[r][i].record(stream)
+    torch.cuda.synchronize()
+    dur = np.array([[starts[r][i].elapsed_time(ends[r][i]) * 1e-3 for i in range(len(mats))] for r in range(n_ev)])
+    kern_s = float(np.median(dur.sum(axis=1)))
+    per_launch_s = kern_s / len(mats)
+    alg_per_launch = total_alg / len(mats)
+    achieved = alg_per_launch / per_launch_s / 1e9
+    big = int(np.argmax([m[3] for m in mats]))
+    log(f"kernel time (events, sum over launches): {1e6 * kern_s:.1f} us/step; "
+        f"largest matrix {1e6 * np.median(dur[:, big]):.1f} us = {mats[big][3] / np.median(dur[:, big]) / 1e9:.0f} GB/s")
+
+    # dense fp16 baseline on the dequantized weights (context: the paper's FP16 comparison)
+    dense = None
+    if not args.no_dense:
+        try:
+            ws = []
+            for Wp, x, y, _ in mats:
+                ws.append(Wp.dequant().half())
+            torch.cuda.synchronize()
+            xs = [m[1].view(1, -1) for m in mats]
+
+            def dense_step():
+                for w, xx in zip(ws, xs):
+                    torch.nn.functional.linear(xx, w)
+            for _ in range(3):
+                dense_step()
+            torch.cuda.synchronize()
+            nd = max(5, args.steps // 10)
+            t0 = time.perf_counter()
+            for _ in range(nd):
+                dense_step()
+            torch.cuda.synchronize()
+            dense_s = (time.perf_counter() - t0) / nd
+            dense = {"us_per_step": round(1e6 * dense_s, 1), "weight_bytes": 2 * total_w,
+                     "speedup_vbq": round(dense_s / (graph_s or eager_s), 2),
+                     "note": "torch F.linear (fp16) over the dequantized weights, eager launches"}
+            del ws
+            torch.cuda.empty_cache()
+            log(f"dense fp16: {1e6 * dense_s:.1f} us/step")
+        except Exception as e:
+            log(f"dense baseline skipped: {e}")
+
+    wall_s = graph_s if graph_s is not None else eager_s
+    value = total_alg / wall_s / 1e9
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(wl)
+        log(f"cpu oracle: {cpu['value']} ms/step ({cpu['sample']})")
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * wall_s, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "precision": "fp16 activations x {1,2,4,8}-bit codes with fp16 group scales, fp32 accumulation",
+        "data": "synthetic (seeded draws; no trained weights)",
+        "config": {"workload": f"{wl.name} decode step (workload {args.workload}): {len(mats)} GEMVs, "
+                               f"{total_w / 1e9:.2f}G weights", "M": 1,
+                   "algorithmic_bytes_per_step": int(total_alg), "blob_bytes": int(blob_bytes),
+                   "timing": "HIP-graph replay of the step" if graph_s is not None else "eager launches"},
+        "us_per_step": round(1e6 * wall_s, 2),
+        "us_per_step_eager": round(1e6 * eager_s, 2),
+        "us_per_step_graph": round(1e6 * graph_s, 2) if graph_s is not None else None,
+        "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": "vbq_mv_kernel<1>", "launches_per_step": len(mats),
+                     "algorithmic_bytes_per_launch": round(alg_per_launch),
+                     "avg_launch_us": round(1e6 * per_launch_s, 3)},
+        "cpu_baseline": cpu,
+        "dense_fp16_baseline": dense,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

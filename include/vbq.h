@@ -131,6 +131,10 @@ typedef struct vbq_pack_opts {
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* vbq_status_string(vbq_status s);
 
+/* Name of the last HIP runtime error that made an entry point of this thread
+ * return VBQ_ERR_HIP ("hipSuccess" if none); static storage, never NULL. */
+const char* vbq_last_hip_error(void);
+
 /* Layout version this library reads and writes. */
 uint32_t vbq_layout_version(void);
 

@@ -5,10 +5,13 @@
 //
 // Work decomposition (layout version 1, include/vbq.h):
 //   * one workgroup (256 lanes, 4 wave64) owns a row tile and walks its
-//     column-chunk units in order;
-//   * per unit it rebuilds, in LDS, the position of every entry of each width
-//     class from the 2-bit width map (ballot-free: word popcounts, a wave scan
-//     and mbcnt), so lanes can be handed 64 consecutive entries of ONE width;
+//     column-chunk units in order; inside a unit each wave owns a contiguous,
+//     word-aligned slice of group columns and works alone until the end of
+//     the tile (no workgroup barrier per unit);
+//   * a wave finds where its entries of each width class start by counting
+//     the class bits of the 2-bit width map before its slice, then rebuilds
+//     in LDS the position of each of its entries (inverse ballot + mbcnt per
+//     map word), so lanes can be handed 64 consecutive entries of ONE width;
 //   * each lane decodes one 64-weight group with width-specific, branch-free
 //     bit tricks: a masked field of codes, read as a pair of fp16 values, is a
 //     power-of-two multiple of the codes, so v_dot2_f32_f16 multiplies two
@@ -17,12 +20,16 @@
 //   * the offset of the offset-binary codes is removed with the group's
 //     activation sum X_j = sum x: sum q x = sum u x - 2^(b-1) X_j (b >= 2),
 //     sum q x = 2 sum u x - X_j (b = 1);
-//   * per-group partial results go to LDS at their (row, column) position and
-//     each row is summed in a fixed order, so results are bitwise repeatable.
+//   * per-group partial results go to LDS at their (row, column) position,
+//     each wave sums its columns row by row, and the four per-wave row sums
+//     are added in wave order: every sum has a fixed order, so results are
+//     bitwise repeatable.
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
+#include <type_traits>
 
 #include "vbq_layout.hpp"
 
@@ -33,8 +40,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
+#ifndef VBQ_MV_WAVES_PER_SIMD
+#define VBQ_MV_WAVES_PER_SIMD 4
+#endif
 constexpr int kWaves = kThreads / 64;
-constexpr int kMaxWords = vbq::kMaxUnitPositions / 64;  // width-map words per plane of a unit
 
 struct DevMatrix {
   const uint32_t* units;
@@ -42,6 +51,7 @@ struct DevMatrix {
   const uint8_t* codes[4];
   const uint16_t* scales[4];
   uint32_t n_entries[4];
+  uint32_t wmap_words;  // 64-bit words in the width-map section
   int32_t N, K, G, R, C, T, U, logR;
 };
 
@@ -51,7 +61,7 @@ struct MvArgs {
   float* y;           // row m at y + m*ldy
   int64_t ldx, ldy;
   int32_t M;          // rows of x actually present (<= MT)
-  int32_t SC;         // group columns per sub-chunk (LDS staging window)
+  int32_t SW;         // group columns per window (LDS staging)
 };
 
 __device__ __forceinline__ half2_t as_h2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
@@ -127,14 +137,38 @@ struct Dec<3> {
   __device__ static constexpr float inv_value(int) { return 16777216.0f; }  // 2^24
 };
 
+// Single-accumulator tables, used when several activation rows share one
+// decode (M >= 4): every field is moved to one target bit, at one extra shift
+// per field, so each row needs one accumulator instead of one per slot.
+template <int CLS>
+struct Dec1;
+template <>
+struct Dec1<0> {  // every bit to the exponent bit 14: (0, 2.0)
+  static constexpr int B = 1, kFields = 16, kSlots = 1;
+  __device__ static constexpr Field field(int f) { return Field{14 - f, 14}; }
+  __device__ static constexpr int slot(int) { return 0; }
+  __device__ static constexpr float inv_value(int) { return 0.5f; }
+};
+template <>
+struct Dec1<1> {  // every field to bits 8-9: u * 2^-16
+  static constexpr int B = 2, kFields = 8, kSlots = 1;
+  __device__ static constexpr Field field(int f) { return Field{8 - 2 * f, 8}; }
+  __device__ static constexpr int slot(int) { return 0; }
+  __device__ static constexpr float inv_value(int) { return 65536.0f; }
+};
+template <>
+struct Dec1<2> : Dec<2> {};
+template <>
+struct Dec1<3> : Dec<3> {};
+
+template <int CLS, int MT>
+using DecFor = typename std::conditional<(MT >= 4), Dec1<CLS>, Dec<CLS>>::type;
+
 // ---------------------------------------------------------------------------
 // Index build: positions of each class's entries inside one unit.
 // ---------------------------------------------------------------------------
 struct UnitInfo {
-  int j0, cols, rows, npos, W;      // first group column, columns, real rows, positions, words/plane
-  uint32_t start[4];               // first global entry of each class
-  int n[4];                        // entries of each class in the unit
-  int base[4];                     // class segment start inside inv[]
+  int j0, cols, rows, npos, W;  // first group column, columns, real rows, positions, words per plane
   uint32_t wmap_word;
 };
 
@@ -173,300 +207,592 @@ __device__ __forceinline__ UnitInfo load_unit(const DevMatrix& mat, int t, int k
   u.rows = min(mat.R, mat.N - t * mat.R);
   u.npos = u.cols * mat.R;
   u.W = (u.npos + 63) >> 6;
-  const uint32_t* row = mat.units + (size_t)unit * vbq::kUnitRowWords;
-  const uint32_t* nxt = row + vbq::kUnitRowWords;
-  int base = 0;
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    u.start[c] = row[c];
-    uint32_t end = nxt[c];
-    // never step outside the class section, whatever the blob says
-    if (end > mat.n_entries[c]) end = mat.n_entries[c];
-    int n = end > u.start[c] ? (int)(end - u.start[c]) : 0;
-    if (n > u.npos - base) n = u.npos - base;  // segments of inv[] stay inside R*C
-    u.n[c] = n;
-    u.base[c] = base;
-    base += n;
-  }
-  u.wmap_word = row[4];
+  u.wmap_word = mat.units[(size_t)unit * vbq::kUnitRowWords + 4];
   return u;
 }
 
-// Builds inv[base[c] + e] = position of the e-th class-c entry, and
-// pre[c][w] = number of class-c entries in words < w (w = 0..W).
-__device__ void build_index(const DevMatrix& mat, const UnitInfo& u, uint16_t* inv, uint16_t (*pre)[kMaxWords + 1]) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const uint64_t* plane0 = mat.wmap + u.wmap_word;
-  const uint64_t* plane1 = plane0 + u.W;
-  // phase A: class counts per word (one thread per word)
-  for (int w = tid; w < u.W; w += kThreads) {
-    uint64_t m[4];
-    class_masks(plane0[w], plane1[w], valid_mask(w, u.npos, mat.R, u.rows), m);
+__device__ __forceinline__ uint32_t lane_id() {
+  return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// ---------------------------------------------------------------------------
+// Work split.  A workgroup owns one row tile; inside each unit of the tile
+// every wave owns a contiguous, width-map-word-aligned slice of the unit's
+// group columns.  Positions are column-major, so a wave's positions are one
+// contiguous run of the unit and its entries of each class are one
+// contiguous run of that class's section: the wave finds where its runs
+// start by counting the class bits of the width-map words before its slice.
+// Everything up to a per-wave row sum is wave-local (x staging, index,
+// decode, partial sums), in a private LDS region of the wave, so no
+// workgroup barrier is needed until the per-wave row sums are combined, in a
+// fixed order, at the end of the tile.  A slice is processed in windows of
+// at most SW columns (the whole slice for one activation row).
+//
+// x is staged column-contiguous with a 144-byte column stride (128 bytes of
+// activations + 16 of padding), so an entry reads its column's 8 chunks at
+// immediate offsets from one address and up to 8 distinct consecutive
+// columns in one instruction fall on distinct banks.
+// ---------------------------------------------------------------------------
+constexpr int kXStride = 144;
+constexpr int kXRegs = 4;  // 16-byte x chunks per lane for one row: windows of <= 32 columns
+
+__host__ __device__ inline int align16(int v) { return (v + 15) & ~15; }
+
+// Byte offsets inside one wave's LDS region (window of SW columns, R rows,
+// MT activation rows).
+struct WavePlan {
+  int inv, xs, Xs, part, bytes;
+};
+
+__host__ __device__ inline WavePlan wave_plan(int R, int SW, int MT) {
+  WavePlan p;
+  int o = 0;
+  p.inv = o;  o += align16(SW * R * 2);  // uint16 local position of each entry
+  p.xs = o;   o += MT * SW * kXStride;   // staged x
+  p.Xs = o;   o += align16(MT * SW * 4); // per-column activation sums
+  p.part = o; o += MT * SW * R * 4;      // per-entry partial products
+  p.bytes = o;
+  return p;
+}
+
+// Whole workgroup: kWaves row-sum arrays (MT*R floats each), then kWaves regions.
+__host__ __device__ inline int mv_lds_bytes(int R, int SW, int MT) {
+  return kWaves * (MT * R * 4 + wave_plan(R, SW, MT).bytes);
+}
+
+// Group columns per width-map word (1 when a column spans whole words).
+__host__ __device__ inline int cols_per_word(int R) { return R >= 64 ? 1 : 64 / R; }
+
+// Columns of the widest wave slice of a unit of C columns.
+__host__ __device__ inline int max_slice_cols(int R, int C) {
+  const int cw = cols_per_word(R);
+  const int per = ((C + cw - 1) / cw + kWaves - 1) / kWaves;
+  return min(C, per * cw);
+}
+
+__device__ __forceinline__ u32x4 lds_u32x4(uint32_t addr) {
+  return *(const __attribute__((address_space(3))) u32x4*)(size_t)addr;
+}
+__device__ __forceinline__ float lds_f32(uint32_t addr) {
+  return *(const __attribute__((address_space(3))) float*)(size_t)addr;
+}
+__device__ __forceinline__ void lds_store_f32(uint32_t addr, float v) {
+  *(__attribute__((address_space(3))) float*)(size_t)addr = v;
+}
+__device__ __forceinline__ void lds_store_u32x4(uint32_t addr, u32x4 v) {
+  *(__attribute__((address_space(3))) u32x4*)(size_t)addr = v;
+}
+__device__ __forceinline__ void lds_store_u16(uint32_t addr, uint16_t v) {
+  *(__attribute__((address_space(3))) uint16_t*)(size_t)addr = v;
+}
+__device__ __forceinline__ int lds_u16(uint32_t addr) {
+  return *(const __attribute__((address_space(3))) uint16_t*)(size_t)addr;
+}
+// Keeps the compiler from moving LDS accesses across phases of a wave that
+// hand data between its lanes through LDS (a wave's LDS operations are
+// executed in order, so no hardware wait is needed).
+__device__ __forceinline__ void lds_phase() { __asm__ __volatile__("" ::: "memory"); }
+
+// Group columns [cb, ce) of unit u owned by `wave`.
+__device__ __forceinline__ void wave_slice(const UnitInfo& u, int R, int wave, int& cb, int& ce) {
+  const int cw = cols_per_word(R);
+  const int per = ((u.cols + cw - 1) / cw + kWaves - 1) / kWaves;
+  cb = min(u.cols, wave * per * cw);
+  ce = min(u.cols, (wave + 1) * per * cw);
+}
+
+__device__ __forceinline__ uint64_t read_lane64(uint64_t v, int l) {
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, l), hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Width-map words 0 .. we-1 of the unit (both planes), lane l holding words
+// l and l + 64.  Loads are unconditional, with indices clamped to the unit
+// and to the section, so outstanding-load counts stay exact.
+struct WmapRegs {
+  uint64_t a0, a1;  // plane 0 / plane 1 of word l
+  uint64_t b0, b1;  // plane 0 / plane 1 of word l + 64
+};
+
+__device__ __forceinline__ WmapRegs load_wmap(const DevMatrix& mat, const UnitInfo& u, int we, uint32_t lane) {
+  const uint32_t last = mat.wmap_words - 1;
+  const uint32_t top = (uint32_t)(max(we, 1) - 1);
+  const uint32_t wa = min(lane, top), wb = min(lane + 64u, top);
+  WmapRegs r;
+  r.a0 = mat.wmap[min(u.wmap_word + wa, last)];
+  r.a1 = mat.wmap[min(u.wmap_word + (uint32_t)u.W + wa, last)];
+  r.b0 = mat.wmap[min(u.wmap_word + wb, last)];
+  r.b1 = mat.wmap[min(u.wmap_word + (uint32_t)u.W + wb, last)];
+  return r;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) pre[c][w + 1] = (uint16_t)__popcll(m[c]);
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  return v;
+}
+
+// Class counts of words [0, wb) of the unit (where the window's runs start
+// inside the unit's class runs) and of words [wb, we) (the window's runs).
+struct WinCounts {
+  uint32_t before[4], own[4];
+};
+
+__device__ __forceinline__ WinCounts window_counts(const WmapRegs& wr, const UnitInfo& u, int wb, int we, int R,
+                                                   uint32_t lane) {
+  uint32_t bef01 = 0, bef23 = 0, own01 = 0, own23 = 0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int w = (int)lane + 64 * h;
+    uint64_t m[4];
+    class_masks(h ? wr.b0 : wr.a0, h ? wr.b1 : wr.a1, valid_mask(w, u.npos, R, u.rows), m);
+    // packed 16-bit halves: a unit has at most 8192 positions
+    const uint32_t c01 = (uint32_t)__popcll(m[0]) | ((uint32_t)__popcll(m[1]) << 16);
+    const uint32_t c23 = (uint32_t)__popcll(m[2]) | ((uint32_t)__popcll(m[3]) << 16);
+    if (w < wb) {
+      bef01 += c01;
+      bef23 += c23;
+    } else if (w < we) {
+      own01 += c01;
+      own23 += c23;
+    }
   }
-  __syncthreads();
-  // phase B: inclusive scan over words, wave 0 (each lane owns two words)
-  if (wave == 0) {
+  bef01 = wave_sum(bef01);
+  bef23 = wave_sum(bef23);
+  own01 = wave_sum(own01);
+  own23 = wave_sum(own23);
+  WinCounts wc;
+  wc.before[0] = uniform(bef01 & 0xFFFF);
+  wc.before[1] = uniform(bef01 >> 16);
+  wc.before[2] = uniform(bef23 & 0xFFFF);
+  wc.before[3] = uniform(bef23 >> 16);
+  wc.own[0] = uniform(own01 & 0xFFFF);
+  wc.own[1] = uniform(own01 >> 16);
+  wc.own[2] = uniform(own23 & 0xFFFF);
+  wc.own[3] = uniform(own23 >> 16);
+  return wc;
+}
+
+// inv[k] (uint16, from byte offset `inv`) = window-local position of the
+// k-th entry of the window, entries ordered by class, then by position.  A
+// word's masks are read into scalar registers, each class's lanes are
+// enabled straight from its mask (inverse ballot) and mbcnt gives the rank.
+__device__ __forceinline__ void build_index(const WmapRegs& wr, const UnitInfo& u, int wb, int we, int R,
+                                            const WinCounts& wc, uint32_t inv, uint32_t lane) {
+  uint32_t run[4];
+  run[0] = 0;
+  run[1] = wc.own[0];
+  run[2] = run[1] + wc.own[1];
+  run[3] = run[2] + wc.own[2];
+  for (int w = wb; w < we; ++w) {
+    const bool hi = w >= 64;
+    const uint64_t p0 = read_lane64(hi ? wr.b0 : wr.a0, w & 63), p1 = read_lane64(hi ? wr.b1 : wr.a1, w & 63);
+    uint64_t m[4];
+    class_masks(p0, p1, valid_mask(w, u.npos, R, u.rows), m);
+    const uint16_t pos = (uint16_t)((w - wb) * 64 + (int)lane);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const int w0 = 2 * lane, w1 = 2 * lane + 1;
-      const int a = w0 < u.W ? pre[c][w0 + 1] : 0;
-      const int b = w1 < u.W ? pre[c][w1 + 1] : 0;
-      int incl = a + b;
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {
-        const int o = __shfl_up(incl, d, 64);
-        if (lane >= d) incl += o;
+      if (m[c]) {
+        if (__builtin_amdgcn_inverse_ballot_w64(m[c]))
+          lds_store_u16(inv + 2u * __builtin_amdgcn_mbcnt_hi((uint32_t)(m[c] >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)m[c], run[c])),
+                        pos);
+        run[c] += (uint32_t)__popcll(m[c]);
       }
-      const int excl = incl - a - b;
-      if (w0 < u.W) pre[c][w0 + 1] = (uint16_t)(excl + a);
-      if (w1 < u.W) pre[c][w1 + 1] = (uint16_t)(excl + a + b);
-      if (lane == 0) pre[c][0] = 0;
     }
   }
-  __syncthreads();
-  // phase C: every wave takes whole words; lanes are positions
-  for (int w = wave; w < u.W; w += kWaves) {
-    uint64_t m[4];
-    const uint64_t p0 = plane0[w], p1 = plane1[w];
-    class_masks(p0, p1, valid_mask(w, u.npos, mat.R, u.rows), m);
-    const int c = (int)((p0 >> lane) & 1) | ((int)((p1 >> lane) & 1) << 1);
-    const uint64_t mine = c == 0 ? m[0] : c == 1 ? m[1] : c == 2 ? m[2] : m[3];
-    if ((mine >> lane) & 1) {
-      const int rank = pre[c][w] + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mine >> 32),
-                                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)mine, 0u));
-      if (rank < u.n[c]) inv[u.base[c] + rank] = (uint16_t)(w * 64 + lane);
-    }
-  }
-  __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
-// Per-class fused decode + multiply for a window of group columns.
+// Batches.  A wave's batch of class CLS holds E entries per lane: 32 bytes of
+// codes per lane for widths up to 4 bits (4 x 1-bit, 2 x 2-bit, 1 x 4-bit)
+// and one 64-byte entry for 8 bits.  Entry e of the window's class run goes
+// to lane e % 64 of group e / 64; batch b covers groups bE .. bE+E-1, so
+// every load instruction reads one contiguous span.
 // ---------------------------------------------------------------------------
-template <int CLS, int MT>
-__device__ __forceinline__ void mv_class(const MvArgs& a, const UnitInfo& u, const uint16_t* inv,
-                                         const uint16_t (*pre)[kMaxWords + 1], int wlo, int whi, int js0,
-                                         int scols, const u32x4* xs, const float* Xs, float* part) {
-  using D = Dec<CLS>;
-  constexpr int NW = 2 * D::B;  // uint32 words per entry
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int e_lo = pre[CLS][wlo], e_hi = min((int)pre[CLS][whi], u.n[CLS]);
-  const uint32_t* codes = (const uint32_t*)a.m.codes[CLS];
-  const uint16_t* scales = a.m.scales[CLS];
-  const int R = a.m.R, logR = a.m.logR;
-  const int plane = scols * R;  // partials per x row in this window
-  for (int e0 = e_lo + wave * 64; e0 < e_hi; e0 += kWaves * 64) {
-    const int e = e0 + lane;
-    if (e >= e_hi) continue;
-    const int p = inv[u.base[CLS] + e];
-    const int js = (p >> logR) - js0;     // column inside the window
-    const int r = p & (R - 1);
-    const size_t g = (size_t)u.start[CLS] + e;
-    uint32_t w[NW];
+constexpr int kBatchWords = 8;
+
+template <int CLS>
+struct Batch {
+  static constexpr int NW = 2 << CLS;                                 // uint32 words per entry
+  static constexpr int E = NW >= kBatchWords ? 1 : kBatchWords / NW;  // entries per lane
+  uint32_t w[E * NW];
+  uint16_t s[E];
+};
+
+// Every lane always loads: lanes past the end re-read the last entry of the
+// run.  Unconditional loads keep the number of outstanding loads the same on
+// every path, so the compiler waits only for the batch it is about to decode
+// and the next batch stays in flight (a conditional load makes it wait for all).
+template <int CLS>
+__device__ __forceinline__ void load_batch(Batch<CLS>& bt, const uint32_t* __restrict__ codes,
+                                           const uint16_t* __restrict__ scales, uint32_t start, int n, int b,
+                                           uint32_t lane) {
+  constexpr int NW = Batch<CLS>::NW, E = Batch<CLS>::E;
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    const int e = min((b * E + i) * 64 + (int)lane, n - 1);
+    const size_t g = (size_t)start + (uint32_t)e;
+    bt.s[i] = scales[g];
     if constexpr (NW == 2) {
       const u32x2 v = __builtin_nontemporal_load((const u32x2*)(codes + g * NW));
-      w[0] = v.x;
-      w[1] = v.y;
+      bt.w[2 * i] = v.x;
+      bt.w[2 * i + 1] = v.y;
     } else {
 #pragma unroll
-      for (int i = 0; i < NW / 4; ++i) {
-        const u32x4 v = __builtin_nontemporal_load((const u32x4*)(codes + g * NW) + i);
-        w[4 * i] = v.x;
-        w[4 * i + 1] = v.y;
-        w[4 * i + 2] = v.z;
-        w[4 * i + 3] = v.w;
+      for (int k = 0; k < NW / 4; ++k) {
+        const u32x4 v = __builtin_nontemporal_load((const u32x4*)(codes + g * NW) + k);
+        bt.w[i * NW + 4 * k] = v.x;
+        bt.w[i * NW + 4 * k + 1] = v.y;
+        bt.w[i * NW + 4 * k + 2] = v.z;
+        bt.w[i * NW + 4 * k + 3] = v.w;
       }
-    }
-    const float s = (float)__builtin_bit_cast(_Float16, scales[g]);
-    float acc[MT][D::kSlots];
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-      for (int k = 0; k < D::kSlots; ++k) acc[m][k] = 0.0f;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {  // x chunk q holds pairs 4q..4q+3
-      u32x4 xv[MT];
-#pragma unroll
-      for (int m = 0; m < MT; ++m) xv[m] = xs[(m * 8 + q) * scols + js];
-#pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) {
-        const int i = 4 * q + c4;                  // pair index
-        const int wi = i / D::kFields, f = i % D::kFields;
-        constexpr uint32_t one = (1u << D::B) - 1;
-        const Field fd = D::field(f);
-        const uint32_t mask = (one << fd.t) * 0x00010001u;
-        const uint32_t v = shl(w[wi], fd.shift) & mask;
-        const int sl = D::slot(fd.t);
-#pragma unroll
-        for (int m = 0; m < MT; ++m) acc[m][sl] = dot2(v, xv[m][c4], acc[m][sl]);
-      }
-    }
-#pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      float su = acc[m][0] * D::inv_value(0);
-#pragma unroll
-      for (int k = 1; k < D::kSlots; ++k) su = __builtin_fmaf(acc[m][k], D::inv_value(k), su);
-      const float X = Xs[m * scols + js];
-      const float sq = CLS == 0 ? __builtin_fmaf(su, 2.0f, -X) : __builtin_fmaf(-(float)(1 << (D::B - 1)), X, su);
-      part[m * plane + js * R + r] = s * sq;
     }
   }
 }
 
-// Stage x for group columns [j0, j0+cols) of every present row into LDS as
-// 16-byte chunks, chunk-major: xs[(m*8 + q)*cols + j] = x[m][(j0+j)*64 + 8q .. +8].
-// Then Xs[m*cols + j] = sum of the 64 activations of column j, in fixed order.
-template <int MT>
-__device__ __forceinline__ void stage_x(const MvArgs& a, int j0, int cols, u32x4* xs, float* Xs) {
-  const int tid = threadIdx.x;
-  const int n = MT * cols * 8;
-  for (int i = tid; i < n; i += kThreads) {
-    const int m = i / (cols * 8), rem = i - m * cols * 8, j = rem >> 3, q = rem & 7;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (m < a.M) v = *(const u32x4*)(a.x + m * a.ldx + (size_t)(j0 + j) * 64 + q * 8);
-    xs[(m * 8 + q) * cols + j] = v;
+struct Win {  // LDS byte addresses of the wave's window buffers
+  uint32_t xs, Xs, part;
+  uint32_t xstride_m;  // bytes between the staged x rows
+  uint32_t part_m;     // bytes between the partial-product planes of two x rows
+  int SW, logR;        // window columns (Xs row stride), log2 R
+};
+
+// Decode one entry (64 weights) at window-local position p, reading the
+// activations of the MT rows from LDS chunk by chunk, and write its partial
+// product(s) to LDS (only lanes with `valid`).
+template <int CLS, int MT>
+__device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits, int p, bool valid,
+                                              const Win& wn) {
+  using D = DecFor<CLS, MT>;
+  const int js = p >> wn.logR;
+  const uint32_t xaddr = wn.xs + (uint32_t)__umul24((uint32_t)js, kXStride);
+  float acc[MT][D::kSlots];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int k = 0; k < D::kSlots; ++k) acc[m][k] = 0.0f;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {  // x chunk q holds pairs 4q..4q+3
+    u32x4 xv[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) xv[m] = lds_u32x4(xaddr + (uint32_t)m * wn.xstride_m + 16u * q);
+#pragma unroll
+    for (int c4 = 0; c4 < 4; ++c4) {
+      const int i = 4 * q + c4;
+      const int wi = i / D::kFields, f = i % D::kFields;
+      constexpr uint32_t one = (1u << D::B) - 1;
+      const Field fd = D::field(f);
+      const uint32_t mask = (one << fd.t) * 0x00010001u;
+      const uint32_t v = shl(w[wi], fd.shift) & mask;
+      const int sl = D::slot(fd.t);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[m][sl] = dot2(v, xv[m][c4], acc[m][sl]);
+    }
   }
-  __syncthreads();
+  const float s = (float)__builtin_bit_cast(_Float16, s_bits);
+  const uint32_t paddr = wn.part + 4u * (uint32_t)p;
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    float su = acc[m][0] * D::inv_value(0);
+#pragma unroll
+    for (int k = 1; k < D::kSlots; ++k) su = __builtin_fmaf(acc[m][k], D::inv_value(k), su);
+    const float X = lds_f32(wn.Xs + 4u * (uint32_t)(m * wn.SW + js));
+    const float sq = CLS == 0 ? __builtin_fmaf(su, 2.0f, -X) : __builtin_fmaf(-(float)(1 << (D::B - 1)), X, su);
+    if (valid) lds_store_f32(paddr + (uint32_t)m * wn.part_m, s * sq);
+  }
+}
+
+template <int CLS, int MT>
+__device__ __forceinline__ void decode_batch(const Batch<CLS>& bt, uint32_t inv_c, int n, int b, uint32_t lane,
+                                             const Win& wn) {
+  constexpr int NW = Batch<CLS>::NW, E = Batch<CLS>::E;
+  int p[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) p[i] = lds_u16(inv_c + 2u * (uint32_t)min((b * E + i) * 64 + (int)lane, n - 1));
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    const int g0 = (b * E + i) * 64;
+    if (g0 < n)  // wave-uniform: whole groups past the end are skipped
+      compute_entry<CLS, MT>(&bt.w[i * NW], bt.s[i], p[i], g0 + (int)lane < n, wn);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// The n entries of class CLS of the window, starting at entry `start` of the
+// class section; the next batch is in flight while the current one is
+// decoded (past the last batch the load repeats the last batch, which keeps
+// the loop free of conditional loads).  If `have`, batch 0 is already in A.
+template <int CLS, int MT>
+__device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS>& A, bool have, uint32_t start, int n,
+                                          uint32_t inv_c, const Win& wn, uint32_t lane) {
+  if (n <= 0) return;
+  const uint32_t* codes = (const uint32_t*)mat.codes[CLS];
+  const uint16_t* scales = mat.scales[CLS];
+  constexpr int per_batch = Batch<CLS>::E * 64;
+  const int nb = (n + per_batch - 1) / per_batch;
+  if (!have) load_batch<CLS>(A, codes, scales, start, n, 0, lane);
+  Batch<CLS> B;
+  for (int b = 0; b < nb; b += 2) {
+    load_batch<CLS>(B, codes, scales, start, n, min(b + 1, nb - 1), lane);
+    decode_batch<CLS, MT>(A, inv_c, n, b, lane, wn);
+    if (b + 1 >= nb) break;
+    load_batch<CLS>(A, codes, scales, start, n, min(b + 2, nb - 1), lane);
+    decode_batch<CLS, MT>(B, inv_c, n, b + 1, lane, wn);
+  }
+}
+
+// x of one activation row for a window of `cols` <= 32 columns starting at
+// group column j: lane l holds 16-byte chunks l, l + 64, ... (clamped loads).
+struct XRegs {
+  u32x4 v[kXRegs];
+};
+
+__device__ __forceinline__ void load_x1(const uint16_t* __restrict__ x, int j, int cols, XRegs& xr, uint32_t lane) {
+  const int n = cols * 8;
+#pragma unroll
+  for (int k = 0; k < kXRegs; ++k) {
+    const int i = min((int)lane + 64 * k, n - 1);
+    xr.v[k] = *(const u32x4*)(x + (size_t)(j + (i >> 3)) * 64 + (i & 7) * 8);
+  }
+}
+
+// Stores the chunks to LDS and writes each column's activation sum: every
+// lane sums its chunk, then the 8 lanes of a column combine their sums with
+// a fixed butterfly (the same value in all 8 lanes).
+__device__ __forceinline__ void store_x1(int cols, const XRegs& xr, const Win& wn, uint32_t lane) {
+  const int n = cols * 8;
   const uint32_t ones = 0x3C003C00u;  // (1.0, 1.0)
-  for (int i = tid; i < MT * cols; i += kThreads) {
-    const int m = i / cols, j = i - m * cols;
+#pragma unroll
+  for (int k = 0; k < kXRegs; ++k) {
+    const int i = (int)lane + 64 * k;
+    if (k * 64 < n) {  // wave-uniform
+      const u32x4 v = xr.v[k];
+      float sum = dot2(v.x, ones, 0.0f);
+      sum = dot2(v.y, ones, sum);
+      sum = dot2(v.z, ones, sum);
+      sum = dot2(v.w, ones, sum);
+      sum += __shfl_xor(sum, 1, 64);
+      sum += __shfl_xor(sum, 2, 64);
+      sum += __shfl_xor(sum, 4, 64);
+      if (i < n) {
+        lds_store_u32x4(wn.xs + (uint32_t)((i >> 3) * kXStride + (i & 7) * 16), v);
+        if ((i & 7) == 0) lds_store_f32(wn.Xs + 4u * (uint32_t)(i >> 3), sum);
+      }
+    }
+  }
+}
+
+// General staging (several activation rows): x rows m < M of columns
+// [j, j + cols) and their column sums (sequential order); rows M..MT-1 are 0.
+template <int MT>
+__device__ __forceinline__ void stage_x(const MvArgs& a, int j, int cols, const Win& wn, uint32_t lane) {
+  const int n = MT * cols * 8;
+  for (int i = (int)lane; i < n; i += 64) {
+    const int m = i / (cols * 8), rem = i - m * (cols * 8);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (m < a.M) v = *(const u32x4*)(a.x + m * a.ldx + (size_t)(j + (rem >> 3)) * 64 + (rem & 7) * 8);
+    lds_store_u32x4(wn.xs + (uint32_t)m * wn.xstride_m + (uint32_t)((rem >> 3) * kXStride + (rem & 7) * 16), v);
+  }
+  lds_phase();
+  const uint32_t ones = 0x3C003C00u;
+  for (int i = (int)lane; i < MT * cols; i += 64) {
+    const int m = i / cols, jc = i - m * cols;
+    const uint32_t base = wn.xs + (uint32_t)m * wn.xstride_m + (uint32_t)(jc * kXStride);
     float acc = 0.0f;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      const u32x4 v = xs[(m * 8 + q) * cols + j];
+      const u32x4 v = lds_u32x4(base + 16u * q);
       acc = dot2(v.x, ones, acc);
       acc = dot2(v.y, ones, acc);
       acc = dot2(v.z, ones, acc);
       acc = dot2(v.w, ones, acc);
     }
-    Xs[i] = acc;
+    lds_store_f32(wn.Xs + 4u * (uint32_t)(m * wn.SW + jc), acc);
   }
-  __syncthreads();
 }
 
-struct LdsPlan {
-  int inv, pre, xs, Xs, part, yacc, red, total;
-};
+// Adds the window's row sums (columns 0..cols-1 in order) to the wave's row
+// sums: lane l owns the (row, x-row) slots l, l + 64, ...
+template <int MT>
+__device__ __forceinline__ void reduce_window(const Win& wn, int R, int cols, int rows, uint32_t ysum,
+                                              uint32_t lane) {
+  for (int slot = (int)lane; slot < MT * R; slot += 64) {
+    const int m = slot >> wn.logR, r = slot & (R - 1);
+    if (r >= rows) continue;
+    const uint32_t base = wn.part + (uint32_t)m * wn.part_m + 4u * (uint32_t)r;
+    float acc = 0.0f;
+    int j = 0;
+    for (; j + 8 <= cols; j += 8) {
+      float v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = lds_f32(base + 4u * (uint32_t)((j + k) * R));
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc += v[k];
+    }
+    for (; j < cols; ++j) acc += lds_f32(base + 4u * (uint32_t)(j * R));
+    const uint32_t ya = ysum + 4u * (uint32_t)slot;
+    lds_store_f32(ya, lds_f32(ya) + acc);
+  }
+}
 
-__host__ __device__ inline int align16(int v) { return (v + 15) & ~15; }
+// Start of unit `unit`'s class-c run in the class section.
+__device__ __forceinline__ uint32_t class_start(const DevMatrix& mat, int unit, int c) {
+  return mat.units[(size_t)unit * vbq::kUnitRowWords + c];
+}
 
-__host__ __device__ inline LdsPlan lds_plan(int R, int C, int MT, int SC) {
-  LdsPlan p;
-  int o = 0;
-  p.inv = o;  o += align16(R * C * 2);
-  p.pre = o;  o += align16(4 * (kMaxWords + 1) * 2);
-  p.xs = o;   o += MT * 8 * SC * 16;
-  p.Xs = o;   o += align16(MT * SC * 4);
-  p.part = o; o += align16(MT * SC * R * 4);
-  p.yacc = o; o += align16(MT * R * 4);
-  p.red = o;  o += kThreads * 4;
-  p.total = o;
-  return p;
+// Entries of a run that stay inside the class section (a malformed blob can
+// make the width map and the unit table disagree).
+__device__ __forceinline__ int clamp_run(const DevMatrix& mat, int c, uint32_t start, uint32_t n) {
+  const uint32_t lim = mat.n_entries[c];
+  return start >= lim ? 0 : (int)min(n, lim - start);
 }
 
 template <int MT>
-__global__ __launch_bounds__(kThreads) void vbq_mv_kernel(MvArgs a) {
+__global__ __launch_bounds__(kThreads, MT == 1 ? VBQ_MV_WAVES_PER_SIMD : 2) void vbq_mv_kernel(MvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const DevMatrix& mat = a.m;
-  const LdsPlan L = lds_plan(mat.R, mat.C, MT, a.SC);
-  uint16_t* inv = (uint16_t*)(smem + L.inv);
-  auto pre = (uint16_t(*)[kMaxWords + 1])(smem + L.pre);
-  u32x4* xs = (u32x4*)(smem + L.xs);
-  float* Xs = (float*)(smem + L.Xs);
-  float* part = (float*)(smem + L.part);
-  float* yacc = (float*)(smem + L.yacc);
-  float* red = (float*)(smem + L.red);
-  const int tid = threadIdx.x;
-  const int R = mat.R;
-  const int NS = MT * R;  // output slots (x row, tile row)
+  const int R = mat.R, SW = a.SW;
+  const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
+  const uint32_t lane = lane_id();
+  const int wave = wave_id();
+  const int t = blockIdx.x;  // one row tile per workgroup
+  const int NS = MT * R;
+  const WavePlan P = wave_plan(R, SW, MT);
+  const uint32_t ysum = lds0 + (uint32_t)(wave * NS * 4);
+  const uint32_t region = lds0 + (uint32_t)(kWaves * NS * 4 + wave * P.bytes);
+  Win wn;
+  wn.xs = region + P.xs;
+  wn.Xs = region + P.Xs;
+  wn.part = region + P.part;
+  wn.xstride_m = (uint32_t)(SW * kXStride);
+  wn.part_m = (uint32_t)(SW * R * 4);
+  wn.SW = SW;
+  wn.logR = mat.logR;
+  const uint32_t inv = region + P.inv;
+  for (int i = (int)lane; i < NS; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
 
-  for (int t = blockIdx.x; t < mat.T; t += gridDim.x) {
-    for (int i = tid; i < NS; i += kThreads) yacc[i] = 0.0f;
-    for (int k = 0; k < mat.U; ++k) {
-      const UnitInfo u = load_unit(mat, t, k);
-      build_index(mat, u, inv, pre);
-      for (int js0 = 0; js0 < u.cols; js0 += a.SC) {
-        const int scols = min(a.SC, u.cols - js0);
-        // words covering positions [js0*R, (js0+scols)*R): SC*R is a multiple of 64
-        const int wlo = (js0 * R) >> 6, whi = min(u.W, ((js0 + scols) * R + 63) >> 6);
-        stage_x<MT>(a, u.j0 + js0, scols, xs, Xs);
-        mv_class<0, MT>(a, u, inv, pre, wlo, whi, js0, scols, xs, Xs, part);
-        mv_class<1, MT>(a, u, inv, pre, wlo, whi, js0, scols, xs, Xs, part);
-        mv_class<2, MT>(a, u, inv, pre, wlo, whi, js0, scols, xs, Xs, part);
-        mv_class<3, MT>(a, u, inv, pre, wlo, whi, js0, scols, xs, Xs, part);
-        __syncthreads();
-        // fixed-order row sums of this window: S threads per slot, then S partials in order
-        const int plane = scols * R;
-        if (NS <= kThreads) {
-          const int S = kThreads / NS;  // NS and kThreads are powers of two
-          const int slot = tid % NS, sub = tid / NS;
-          const int m = slot / R, r = slot % R;
-          float acc = 0.0f;
-          if (r < u.rows)
-            for (int j = sub; j < scols; j += S) acc += part[m * plane + j * R + r];
-          red[tid] = acc;
-          __syncthreads();
-          if (tid < NS && r < u.rows) {
-            float tot = 0.0f;
-            for (int s2 = 0; s2 < S; ++s2) tot += red[s2 * NS + slot];
-            yacc[slot] += tot;
-          }
-        } else {
-          for (int slot = tid; slot < NS; slot += kThreads) {
-            const int m = slot / R, r = slot % R;
-            if (r >= u.rows) continue;
-            float acc = 0.0f;
-            for (int j = 0; j < scols; ++j) acc += part[m * plane + j * R + r];
-            yacc[slot] += acc;
-          }
-        }
-        __syncthreads();
+  for (int k = 0; k < mat.U; ++k) {
+    const UnitInfo u = load_unit(mat, t, k);
+    const int unit = t * mat.U + k;
+    int cb, ce;
+    wave_slice(u, R, wave, cb, ce);
+    if (cb >= ce) continue;  // wave-uniform: this wave has no columns here
+    const int slice_we = (ce * R + 63) >> 6;
+    uint32_t ustart[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) ustart[c] = class_start(mat, unit, c);
+    XRegs xr;
+    if constexpr (MT == 1) load_x1(a.x, u.j0 + cb, ce - cb, xr, lane);  // before the map: one latency
+    const WmapRegs wr = load_wmap(mat, u, slice_we, lane);
+    auto window = [&](int c0, int c1) __attribute__((always_inline)) {
+      const int cols = c1 - c0;
+      const int wb = (c0 * R) >> 6, we = (c1 * R + 63) >> 6;
+      const WinCounts wc = window_counts(wr, u, wb, we, R, lane);
+      uint32_t start[4], seg[4];
+      int n[4];
+      uint32_t o = 0;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        start[c] = ustart[c] + wc.before[c];
+        n[c] = clamp_run(mat, c, start[c], wc.own[c]);
+        seg[c] = inv + 2u * o;
+        o += wc.own[c];
       }
+      // the first batch of 1-bit codes is in flight while x is staged and the index built
+      Batch<0> A0;
+      const bool have0 = n[0] > 0;
+      if (have0) load_batch<0>(A0, (const uint32_t*)mat.codes[0], mat.scales[0], start[0], n[0], 0, lane);
+      build_index(wr, u, wb, we, R, wc, inv, lane);
+      if constexpr (MT == 1)
+        store_x1(cols, xr, wn, lane);
+      else
+        stage_x<MT>(a, u.j0 + c0, cols, wn, lane);
+      lds_phase();
+      run_class<0, MT>(mat, A0, have0, start[0], n[0], seg[0], wn, lane);
+      { Batch<1> A; run_class<1, MT>(mat, A, false, start[1], n[1], seg[1], wn, lane); }
+      { Batch<2> A; run_class<2, MT>(mat, A, false, start[2], n[2], seg[2], wn, lane); }
+      { Batch<3> A; run_class<3, MT>(mat, A, false, start[3], n[3], seg[3], wn, lane); }
+      lds_phase();
+      reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
+      lds_phase();
+    };
+    if constexpr (MT == 1) {
+      window(cb, ce);  // one row: the window is the whole slice
+    } else {
+      for (int c0 = cb; c0 < ce; c0 += SW) window(c0, min(ce, c0 + SW));
     }
-    const int rows = min(R, mat.N - t * R);
-    for (int slot = tid; slot < NS; slot += kThreads) {
-      const int m = slot / R, r = slot % R;
-      if (m < a.M && r < rows) a.y[m * a.ldy + (size_t)t * R + r] = yacc[slot];
+  }
+  __syncthreads();
+  const int rows = min(R, mat.N - t * R);
+  for (int slot = threadIdx.x; slot < NS; slot += kThreads) {
+    const int m = slot >> mat.logR, r = slot & (R - 1);
+    if (m < a.M && r < rows) {
+      float tot = 0.0f;
+#pragma unroll
+      for (int w2 = 0; w2 < kWaves; ++w2) tot += lds_f32(lds0 + 4u * (uint32_t)(w2 * NS + slot));
+      a.y[m * a.ldy + (size_t)t * R + r] = tot;
     }
-    __syncthreads();
   }
 }
 
-// w_hat = s*q written densely, one lane per entry (checking aid, not a hot path).
-__global__ __launch_bounds__(kThreads) void vbq_dequant_kernel(DevMatrix mat, float* W) {
+// w_hat = s*q written densely (checking aid, not a hot path): each wave
+// indexes its slice (one window) and writes its entries, one lane per entry.
+__global__ __launch_bounds__(kThreads) void vbq_dequant_kernel(DevMatrix mat, float* W, int region_bytes) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  uint16_t* inv = (uint16_t*)smem;
-  auto pre = (uint16_t(*)[kMaxWords + 1])(smem + align16(mat.R * mat.C * 2));
-  for (int t = blockIdx.x; t < mat.T; t += gridDim.x) {
-    for (int k = 0; k < mat.U; ++k) {
-      const UnitInfo u = load_unit(mat, t, k);
-      build_index(mat, u, inv, pre);
-      for (int c = 0; c < 4; ++c) {
-        const int B = 1 << c, NW = 2 * B, per = 16 / B;
-        const uint32_t mask = (1u << B) - 1;
-        for (int e = threadIdx.x; e < u.n[c]; e += kThreads) {
-          const int p = inv[u.base[c] + e];
-          const int jl = p >> mat.logR, r = p & (mat.R - 1);
-          const size_t g = (size_t)u.start[c] + e;
-          const uint32_t* wv = (const uint32_t*)mat.codes[c] + g * NW;
-          const float s = (float)__builtin_bit_cast(_Float16, mat.scales[c][g]);
-          float* dst = W + ((size_t)t * mat.R + r) * mat.K + (size_t)(u.j0 + jl) * 64;
-          for (int i = 0; i < 32; ++i) {
-            const uint32_t word = wv[i / per];
-            const int f = i % per;
-            const int u0 = (int)((word >> (f * B)) & mask), u1 = (int)((word >> (16 + f * B)) & mask);
-            const int q0 = c == 0 ? 2 * u0 - 1 : u0 - (1 << (B - 1));
-            const int q1 = c == 0 ? 2 * u1 - 1 : u1 - (1 << (B - 1));
-            dst[2 * i] = s * (float)q0;
-            dst[2 * i + 1] = s * (float)q1;
-          }
+  const uint32_t lane = lane_id();
+  const int wave = wave_id();
+  const int t = blockIdx.x;
+  const int R = mat.R;
+  const uint32_t inv = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem + (uint32_t)(wave * region_bytes);
+  for (int k = 0; k < mat.U; ++k) {
+    const UnitInfo u = load_unit(mat, t, k);
+    const int unit = t * mat.U + k;
+    int cb, ce;
+    wave_slice(u, R, wave, cb, ce);
+    if (cb >= ce) continue;
+    const int wb = (cb * R) >> 6, we = (ce * R + 63) >> 6;
+    const WmapRegs wr = load_wmap(mat, u, we, lane);
+    const WinCounts wc = window_counts(wr, u, wb, we, R, lane);
+    build_index(wr, u, wb, we, R, wc, inv, lane);
+    lds_phase();
+    uint32_t seg = inv;
+    for (int c = 0; c < 4; ++c) {
+      const int B = 1 << c, NW = 2 * B, per = 16 / B;
+      const uint32_t mask = (1u << B) - 1;
+      const uint32_t start = class_start(mat, unit, c) + wc.before[c];
+      const int n = clamp_run(mat, c, start, wc.own[c]);
+      for (int e = (int)lane; e < n; e += 64) {
+        const int p = lds_u16(seg + 2u * (uint32_t)e) + wb * 64;  // unit position
+        const int jl = p >> mat.logR, r = p & (R - 1);
+        const size_t g = (size_t)start + e;
+        const uint32_t* wv = (const uint32_t*)mat.codes[c] + g * NW;
+        const float s = (float)__builtin_bit_cast(_Float16, mat.scales[c][g]);
+        float* dst = W + ((size_t)t * R + r) * mat.K + (size_t)(u.j0 + jl) * 64;
+        for (int i = 0; i < 32; ++i) {
+          const uint32_t word = wv[i / per];
+          const int f = i % per;
+          const int u0 = (int)((word >> (f * B)) & mask), u1 = (int)((word >> (16 + f * B)) & mask);
+          const int q0 = c == 0 ? 2 * u0 - 1 : u0 - (1 << (B - 1));
+          const int q1 = c == 0 ? 2 * u1 - 1 : u1 - (1 << (B - 1));
+          dst[2 * i] = s * (float)q0;
+          dst[2 * i + 1] = s * (float)q1;
         }
       }
-      __syncthreads();
+      seg += 2u * wc.own[c];
     }
+    lds_phase();
   }
+}
+
+thread_local hipError_t g_last_hip_error = hipSuccess;
+
+vbq_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return VBQ_OK;
+  g_last_hip_error = e;
+  return VBQ_ERR_HIP;
 }
 
 vbq_status make_dev_matrix(const vbq_desc* d, const void* blob, DevMatrix* m) {
@@ -482,6 +808,8 @@ vbq_status make_dev_matrix(const vbq_desc* d, const void* blob, DevMatrix* m) {
     m->scales[c] = (const uint16_t*)(b + d->section_off[VBQ_SEC_SCALES0 + c]);
     m->n_entries[c] = (uint32_t)d->n_entries[c];
   }
+  m->wmap_words = (uint32_t)(d->section_len[VBQ_SEC_WMAP] / 8);
+  if (m->wmap_words == 0) return VBQ_ERR_DESC;
   m->N = (int32_t)d->N;
   m->K = (int32_t)d->K;
   m->G = (int32_t)(d->K / 64);
@@ -497,17 +825,19 @@ vbq_status make_dev_matrix(const vbq_desc* d, const void* blob, DevMatrix* m) {
 
 constexpr int kLdsLimit = 160 * 1024;
 
-// Largest sub-chunk (group columns staged at once) that fits the LDS budget,
-// keeping sub-chunk boundaries on width-map word boundaries (SC*R % 64 == 0).
-int choose_sc(int R, int C, int MT) {
-  const int step = R >= 64 ? 1 : 64 / R;
-  for (int sc = C; sc >= 1; --sc) {
-    if (sc != C && sc % step) continue;
-    if (lds_plan(R, C, MT, sc).total <= 64 * 1024) return sc;
-  }
-  for (int sc = C; sc >= 1; --sc) {
-    if (sc != C && sc % step) continue;
-    if (lds_plan(R, C, MT, sc).total <= kLdsLimit) return sc;
+// Window columns for MT activation rows: the whole wave slice if it fits the
+// LDS budget (64 KB, else the 160 KB of a CU), else the largest multiple of
+// the columns per width-map word that does.  One row keeps x of a window in
+// registers and always takes the whole slice (at most 32 columns, since
+// C <= 128 and a slice is a quarter of the unit rounded up to whole words).
+int choose_window(int R, int C, int MT) {
+  const int cw = cols_per_word(R);
+  const int full = max_slice_cols(R, C);
+  if (MT == 1) return full <= kXRegs * 8 && mv_lds_bytes(R, full, 1) <= kLdsLimit ? full : 0;
+  for (int limit : {64 * 1024, kLdsLimit}) {
+    if (mv_lds_bytes(R, full, MT) <= limit) return full;
+    for (int sw = (full / cw) * cw; sw >= cw; sw -= cw)
+      if (mv_lds_bytes(R, sw, MT) <= limit) return sw;
   }
   return 0;
 }
@@ -521,23 +851,32 @@ vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
   a.ldx = ldx;
   a.ldy = ldy;
   a.M = M;
-  a.SC = choose_sc(m.R, m.C, MT);
-  if (a.SC <= 0) return VBQ_ERR_UNSUPPORTED;
-  const int lds = lds_plan(m.R, m.C, MT, a.SC).total;
-  static bool attr_set = false;  // raise the dynamic LDS limit once per process
-  if (!attr_set) {
-    if (hipFuncSetAttribute((const void*)vbq_mv_kernel<MT>, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit) !=
-        hipSuccess)
-      return VBQ_ERR_HIP;
-    attr_set = true;
+  a.SW = choose_window(m.R, m.C, MT);
+  if (a.SW <= 0) return VBQ_ERR_UNSUPPORTED;
+  const int lds = mv_lds_bytes(m.R, a.SW, MT);
+  if (lds > 64 * 1024) {  // beyond the default dynamic LDS limit: raise it once per device
+    static std::atomic<uint64_t> attr_set{0};
+    int dev = 0;
+    vbq_status st = hip_status(hipGetDevice(&dev));
+    if (st != VBQ_OK) return st;
+    const uint64_t bit = 1ull << (dev & 63);
+    if (!(attr_set.load(std::memory_order_acquire) & bit)) {
+      st = hip_status(
+          hipFuncSetAttribute((const void*)vbq_mv_kernel<MT>, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit));
+      if (st != VBQ_OK) return st;
+      attr_set.fetch_or(bit, std::memory_order_release);
+    }
   }
-  hipLaunchKernelGGL(vbq_mv_kernel<MT>, dim3((unsigned)m.T), dim3(kThreads), lds, s, a);
-  return hipGetLastError() == hipSuccess ? VBQ_OK : VBQ_ERR_HIP;
+  void* kargs[] = {&a};
+  return hip_status(
+      hipLaunchKernel((const void*)vbq_mv_kernel<MT>, dim3((unsigned)m.T), dim3(kThreads), kargs, (size_t)lds, s));
 }
 
 }  // namespace
 
 extern "C" {
+
+const char* vbq_last_hip_error(void) { return hipGetErrorName(g_last_hip_error); }
 
 vbq_status vbq_gemv(const vbq_desc* desc, const void* blob_dev, const void* x_dev, float* y_dev, void* stream) {
   if (!x_dev || !y_dev) return VBQ_ERR_NULL;
@@ -573,9 +912,14 @@ vbq_status vbq_dequant(const vbq_desc* desc, const void* blob_dev, float* W_dev,
   vbq_status st = make_dev_matrix(desc, blob_dev, &m);
   if (st != VBQ_OK) return st;
   if ((uintptr_t)W_dev % 4) return VBQ_ERR_BUFFER;
-  const int lds = align16(m.R * m.C * 2) + align16(4 * (kMaxWords + 1) * 2);
-  hipLaunchKernelGGL(vbq_dequant_kernel, dim3((unsigned)m.T), dim3(kThreads), lds, (hipStream_t)stream, m, W_dev);
-  return hipGetLastError() == hipSuccess ? VBQ_OK : VBQ_ERR_HIP;
+  // one uint16 per position of the widest wave slice, rounded up to whole words
+  const int cw = cols_per_word(m.R);
+  const int slice = ((max_slice_cols(m.R, m.C) + cw - 1) / cw) * cw;
+  int region = align16(((slice * m.R + 63) / 64) * 64 * 2);
+  void* args[] = {&m, &W_dev, &region};
+  const int lds = kWaves * region;
+  return hip_status(hipLaunchKernel((const void*)vbq_dequant_kernel, dim3((unsigned)m.T), dim3(kThreads), args,
+                                    (size_t)lds, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -18,7 +18,33 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_02893_amd.build` "
                       "(or __graft_entry__.build()); there is no fallback path")
 
+try:
+    # torch carries its own HIP runtime (SONAME libamdhip64.so.7).  Loading it
+    # first makes libvbq bind to that same runtime, so device pointers and
+    # stream handles from torch are valid in libvbq's calls.
+    import torch as _torch  # noqa: F401
+except ImportError:  # host-only use (packing) works with the system runtime
+    _torch = None
+
 _lib = ctypes.CDLL(LIB_PATH)
+
+
+def hip_runtimes():
+    """Paths of every HIP runtime library mapped into this process."""
+    paths = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                if "libamdhip64" in line:
+                    paths.add(os.path.realpath(line.split()[-1]))
+    except OSError:
+        pass
+    return paths
+
+
+if len(hip_runtimes()) > 1:
+    raise ImportError(f"two HIP runtimes are loaded ({sorted(hip_runtimes())}); import torch before any other "
+                      "HIP library so that libvbq binds to torch's runtime")
 
 MAGIC = 0x31514256
 LAYOUT_VERSION = 1
@@ -28,7 +54,7 @@ STATUS = {0: "VBQ_OK", 1: "VBQ_ERR_NULL", 2: "VBQ_ERR_SHAPE", 3: "VBQ_ERR_BITS",
           5: "VBQ_ERR_NONFINITE", 6: "VBQ_ERR_SCALE_RANGE", 7: "VBQ_ERR_BUFFER", 8: "VBQ_ERR_DESC",
           9: "VBQ_ERR_HIP", 10: "VBQ_ERR_UNSUPPORTED"}
 # exported symbols, in the order include/vbq.h declares them
-EXPORTS = ("vbq_status_string", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
+EXPORTS = ("vbq_status_string", "vbq_last_hip_error", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
            "vbq_desc_check", "vbq_gemv", "vbq_gemm_small", "vbq_dequant")
 
 
@@ -58,6 +84,8 @@ class VbqPackOpts(ctypes.Structure):
 _P = ctypes.c_void_p
 _lib.vbq_status_string.restype = ctypes.c_char_p
 _lib.vbq_status_string.argtypes = [ctypes.c_int]
+_lib.vbq_last_hip_error.restype = ctypes.c_char_p
+_lib.vbq_last_hip_error.argtypes = []
 _lib.vbq_layout_version.restype = ctypes.c_uint32
 _lib.vbq_layout_version.argtypes = []
 _lib.vbq_pack_size.restype = ctypes.c_int
@@ -84,6 +112,8 @@ class VbqError(RuntimeError):
     def __init__(self, status, where):
         self.status = status
         msg = _lib.vbq_status_string(status).decode()
+        if status == 9:
+            msg += f": {_lib.vbq_last_hip_error().decode()}"
         super().__init__(f"{where}: {STATUS.get(status, status)} ({msg})")
 
 

@@ -198,3 +198,8 @@ def test_null_and_buffer_errors():
     assert lib.vbq_gemm_small(ctypes.byref(good), ctypes.c_void_p(256), 0, None, 128, None, 2, None) == 0
     assert lib.vbq_gemv(ctypes.byref(good), ctypes.c_void_p(100), ctypes.c_void_p(256), ctypes.c_void_p(256),
                         None) == 7
+
+
+def test_single_hip_runtime():
+    """libvbq must share torch's HIP runtime: one libamdhip64 in the process."""
+    assert len(vbq.hip_runtimes()) == 1
