@@ -31,6 +31,67 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0
 METRIC = "fused dequant-GEMV effective HBM GB/s (% of peak) and µs per decode step"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_02893_amd", "csrc", "vbq_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "vbq_mv_kernel_9b_step_traffic.md")
+CALIB_BYTES = 256 << 20  # plain copy used to scale the HBM byte counters
+
+
+def kernel_source_hash():
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per GEMV launch from the committed counter summary, or None
+    when that summary is missing or was taken on another kernel source."""
+    try:
+        fields = {}
+        with open(TRAFFIC_FILE) as f:
+            for line in f:
+                if ":" in line and line.startswith("- "):
+                    k, v = line[2:].split(":", 1)
+                    fields[k.strip()] = v.strip().strip("`")
+        if fields.get("kernel_source_sha256") != kernel_source_hash():
+            return None
+        return int(fields["hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def pmc_summary(fetch_dir, write_dir):
+    """Summarise two rocprofv3 --pmc runs of `bench.py --profile` (FETCH_SIZE,
+    then WRITE_SIZE): per-launch KiB of the GEMV kernel, scaled by what the
+    same counters read for the calibration copy of CALIB_BYTES."""
+    import csv
+    import glob
+
+    def per_kernel(d, counter):
+        path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        acc = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            key = "vbq" if "vbq_mv_kernel" in name else ("copy" if "MulFunctor" in name else None)
+            if key is None:
+                continue
+            acc.setdefault(key, {}).setdefault(r["Dispatch_Id"], 0.0)
+            acc[key][r["Dispatch_Id"]] += float(r["Counter_Value"])
+        return {k: list(v.values()) for k, v in acc.items()}
+
+    f, w = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+    calib_kib = CALIB_BYTES / 1024.0
+    f_copy, w_copy = float(np.median(f["copy"])), float(np.median(w["copy"]))
+    f_scale, w_scale = calib_kib / f_copy, calib_kib / w_copy
+    fv, wv = np.array(f["vbq"]), np.array(w["vbq"])
+    fetch_b = float(np.mean(fv)) * f_scale * 1024
+    write_b = float(np.mean(wv)) * w_scale * 1024
+    return {"launches": int(fv.size), "fetch_kib_per_launch_raw": float(np.mean(fv)),
+            "write_kib_per_launch_raw": float(np.mean(wv)), "copy_fetch_kib": f_copy, "copy_write_kib": w_copy,
+            "fetch_scale": f_scale, "write_scale": w_scale, "fetch_bytes_per_launch": fetch_b,
+            "write_bytes_per_launch": write_b, "hbm_bytes_per_launch": int(round(fetch_b + write_b)),
+            "kernel_source_sha256": kernel_source_hash()}
 
 
 def log(msg):
@@ -120,7 +181,12 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 (eager launches only)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc runs of --profile (FETCH_SIZE, WRITE_SIZE) and exit")
     args = ap.parse_args()
+    if args.pmc_summary:
+        print(json.dumps(pmc_summary(*args.pmc_summary)), flush=True)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the fused GEMV path has no multi-GPU mode in this build "
               "(the row / K split that would shard it is described in the design notes).", file=sys.stderr)
@@ -171,20 +237,35 @@ def main():
         torch.cuda.synchronize()
         dt = (time.perf_counter() - t0) / args.steps
         log(f"profile run: {args.steps} eager steps, {1e6 * dt:.1f} us/step")
+        # calibration: a plain copy of known size for the HBM byte counters
+        src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
         print(json.dumps({"profile_run": True, "us_per_step_eager": round(1e6 * dt, 2)}), flush=True)
         return
 
-    # eager timing
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    eager_s = (time.perf_counter() - t0) / args.steps
-    log(f"eager: {1e6 * eager_s:.1f} us/step")
+    def timed(run, n):
+        """Wall time per step (host clock, synchronized on both sides) and GPU
+        time per step (HIP events recorded on the launch stream around the
+        same region)."""
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(n):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / n, e0.elapsed_time(e1) * 1e-3 / n
 
-    # graph timing (same launches captured once, replayed)
-    graph_s = None
+    # eager timing
+    eager_s, eager_gpu_s = timed(step, args.steps)
+    log(f"eager: {1e6 * eager_s:.1f} us/step (events {1e6 * eager_gpu_s:.1f})")
+
+    # graph timing (same launches captured once, replayed on the same stream)
+    graph_s = graph_gpu_s = None
     try:
         g = torch.cuda.CUDAGraph()
         cap = torch.cuda.Stream()
@@ -200,13 +281,8 @@ def main():
         stream.wait_stream(cap)
         for _ in range(args.warmup):
             g.replay()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            g.replay()
-        torch.cuda.synchronize()
-        graph_s = (time.perf_counter() - t0) / args.steps
-        log(f"graph: {1e6 * graph_s:.1f} us/step")
+        graph_s, graph_gpu_s = timed(g.replay, args.steps)
+        log(f"graph: {1e6 * graph_s:.1f} us/step (events {1e6 * graph_gpu_s:.1f})")
         # graph result equals eager result
         ref = [m[2].clone() for m in mats[:3] + mats[-1:]]
         step()
@@ -216,7 +292,15 @@ def main():
     except Exception as e:  # graph capture is an optimisation of the same launches
         log(f"graph capture unavailable: {e}")
 
-    # per-launch kernel durations with events on the launch stream
+    wall_s = graph_s if graph_s is not None else eager_s
+    gpu_s = graph_gpu_s if graph_gpu_s is not None else eager_gpu_s
+    # Every launch of the step is the same kernel and they run back to back,
+    # so its average launch duration is the step's GPU time / launches.
+    per_launch_s = gpu_s / len(mats)
+    alg_per_launch = total_alg / len(mats)
+    achieved = alg_per_launch / per_launch_s / 1e9
+
+    # per-matrix breakdown (diagnostic; each launch bracketed by its own events)
     n_ev = min(5, args.steps)
     starts = [[torch.cuda.Event(enable_timing=True) for _ in mats] for _ in range(n_ev)]
     ends = [[torch.cuda.Event(enable_timing=True) for _ in mats] for _ in range(n_ev)]
@@ -226,14 +310,18 @@ def main():
             vbq.raw_gemv(d, b, x, y, sptr)
             ends[r][i].record(stream)
     torch.cuda.synchronize()
-    dur = np.array([[starts[r][i].elapsed_time(ends[r][i]) * 1e-3 for i in range(len(mats))] for r in range(n_ev)])
-    kern_s = float(np.median(dur.sum(axis=1)))
-    per_launch_s = kern_s / len(mats)
-    alg_per_launch = total_alg / len(mats)
-    achieved = alg_per_launch / per_launch_s / 1e9
-    big = int(np.argmax([m[3] for m in mats]))
-    log(f"kernel time (events, sum over launches): {1e6 * kern_s:.1f} us/step; "
-        f"largest matrix {1e6 * np.median(dur[:, big]):.1f} us = {mats[big][3] / np.median(dur[:, big]) / 1e9:.0f} GB/s")
+    dur = np.median(np.array([[starts[r][i].elapsed_time(ends[r][i]) * 1e-3 for i in range(len(mats))]
+                              for r in range(n_ev)]), axis=0)
+    per_shape = {}
+    for i, (Wp, _, _, alg) in enumerate(mats):
+        key = f"{Wp.desc.N}x{Wp.desc.K}"
+        e = per_shape.setdefault(key, {"count": 0, "us": [], "alg_bytes": alg})
+        e["count"] += 1
+        e["us"].append(1e6 * dur[i])
+    per_shape = {k: {"count": v["count"], "us_median": round(float(np.median(v["us"])), 2),
+                     "GBps": round(v["alg_bytes"] / (1e-6 * float(np.median(v["us"]))) / 1e9, 1)}
+                 for k, v in per_shape.items()}
+    log(f"per shape (launch bracketed by events): {per_shape}")
 
     # dense fp16 baseline on the dequantized weights (context: the paper's FP16 comparison)
     dense = None
@@ -266,7 +354,7 @@ def main():
         except Exception as e:
             log(f"dense baseline skipped: {e}")
 
-    wall_s = graph_s if graph_s is not None else eager_s
+    traffic = measured_traffic()
     value = total_alg / wall_s / 1e9
     cpu = None
     if not args.no_cpu:
@@ -295,10 +383,14 @@ def main():
         "us_per_step_graph": round(1e6 * graph_s, 2) if graph_s is not None else None,
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                      "kernel": "vbq_mv_kernel<1>", "launches_per_step": len(mats),
                      "algorithmic_bytes_per_launch": round(alg_per_launch),
-                     "avg_launch_us": round(1e6 * per_launch_s, 3)},
+                     "avg_launch_us": round(1e6 * per_launch_s, 3),
+                     "timing": "HIP events on the launch stream around the timed region / launches",
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "traffic_vs_algorithmic": round(traffic / alg_per_launch, 3) if traffic else None},
+        "per_shape": per_shape,
         "cpu_baseline": cpu,
         "dense_fp16_baseline": dense,
     }

@@ -39,11 +39,6 @@ typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kThreads = 256;
-#ifndef VBQ_MV_WAVES_PER_SIMD
-#define VBQ_MV_WAVES_PER_SIMD 4
-#endif
-constexpr int kWaves = kThreads / 64;
 
 struct DevMatrix {
   const uint32_t* units;
@@ -51,7 +46,11 @@ struct DevMatrix {
   const uint8_t* codes[4];
   const uint16_t* scales[4];
   uint32_t n_entries[4];
-  uint32_t wmap_words;  // 64-bit words in the width-map section
+  uint32_t last_entry[4];  // load clamp: n_entries - 1 (0 for an empty class, whose pointers then
+                           // name the unit table so that clamped loads stay inside the blob)
+  uint32_t wmap_words;     // 64-bit words in the width-map section
+  uint32_t tile_words;     // width-map words of one row tile (all its units, both planes)
+  uint32_t chunk_words;    // width-map words per plane of a unit with C columns
   int32_t N, K, G, R, C, T, U, logR;
 };
 
@@ -61,6 +60,7 @@ struct MvArgs {
   float* y;           // row m at y + m*ldy
   int64_t ldx, ldy;
   int32_t M;          // rows of x actually present (<= MT)
+  int32_t S;          // slices per unit
   int32_t SW;         // group columns per window (LDS staging)
 };
 
@@ -201,13 +201,15 @@ __device__ __forceinline__ void class_masks(uint64_t p0, uint64_t p1, uint64_t v
 
 __device__ __forceinline__ UnitInfo load_unit(const DevMatrix& mat, int t, int k) {
   UnitInfo u;
-  const int unit = t * mat.U + k;
   u.j0 = k * mat.C;
   u.cols = min(mat.C, mat.G - u.j0);
   u.rows = min(mat.R, mat.N - t * mat.R);
   u.npos = u.cols * mat.R;
   u.W = (u.npos + 63) >> 6;
-  u.wmap_word = mat.units[(size_t)unit * vbq::kUnitRowWords + 4];
+  // units are stored tile by tile and only a tile's last chunk can be narrower,
+  // so the first map word follows from the geometry (no unit-table read on the
+  // path to the first load)
+  u.wmap_word = (uint32_t)t * mat.tile_words + 2u * (uint32_t)k * mat.chunk_words;
   return u;
 }
 
@@ -218,17 +220,18 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // ---------------------------------------------------------------------------
-// Work split.  A workgroup owns one row tile; inside each unit of the tile
-// every wave owns a contiguous, width-map-word-aligned slice of the unit's
-// group columns.  Positions are column-major, so a wave's positions are one
-// contiguous run of the unit and its entries of each class are one
-// contiguous run of that class's section: the wave finds where its runs
-// start by counting the class bits of the width-map words before its slice.
-// Everything up to a per-wave row sum is wave-local (x staging, index,
-// decode, partial sums), in a private LDS region of the wave, so no
-// workgroup barrier is needed until the per-wave row sums are combined, in a
-// fixed order, at the end of the tile.  A slice is processed in windows of
-// at most SW columns (the whole slice for one activation row).
+// Work split.  A workgroup of NW waves owns one row tile.  Each unit of the
+// tile is cut into S slices (contiguous, width-map-word-aligned runs of group
+// columns) and the U*S (unit, slice) items are dealt to the waves in turn.
+// Positions are column-major, so a slice's positions are one contiguous run
+// of the unit and its entries of each class are one contiguous run of that
+// class's section: a wave finds where its runs start by counting the class
+// bits of the width-map words before its slice.  Everything up to a per-wave
+// row sum is wave-local (x staging, index, decode, partial sums), in a
+// private LDS region of the wave, so no workgroup barrier is needed until the
+// per-wave row sums are combined, in wave order, at the end of the tile.
+// A slice is processed in windows of at most SW columns (one window for one
+// activation row).
 //
 // x is staged column-contiguous with a 144-byte column stride (128 bytes of
 // activations + 16 of padding), so an entry reads its column's 8 chunks at
@@ -257,19 +260,27 @@ __host__ __device__ inline WavePlan wave_plan(int R, int SW, int MT) {
   return p;
 }
 
-// Whole workgroup: kWaves row-sum arrays (MT*R floats each), then kWaves regions.
-__host__ __device__ inline int mv_lds_bytes(int R, int SW, int MT) {
-  return kWaves * (MT * R * 4 + wave_plan(R, SW, MT).bytes);
+// Whole workgroup: NW row-sum arrays (MT*R floats each), then NW regions.
+__host__ __device__ inline int mv_lds_bytes(int R, int SW, int MT, int NW) {
+  return NW * (MT * R * 4 + wave_plan(R, SW, MT).bytes);
 }
 
 // Group columns per width-map word (1 when a column spans whole words).
 __host__ __device__ inline int cols_per_word(int R) { return R >= 64 ? 1 : 64 / R; }
 
-// Columns of the widest wave slice of a unit of C columns.
-__host__ __device__ inline int max_slice_cols(int R, int C) {
+// Columns [cb, ce) of slice s of S of a unit with `cols` columns.
+__host__ __device__ inline void slice_cols(int cols, int R, int s, int S, int& cb, int& ce) {
   const int cw = cols_per_word(R);
-  const int per = ((C + cw - 1) / cw + kWaves - 1) / kWaves;
-  return min(C, per * cw);
+  const int per = ((cols + cw - 1) / cw + S - 1) / S;
+  cb = min(cols, s * per * cw);
+  ce = min(cols, (s + 1) * per * cw);
+}
+
+// Columns of the widest slice of a unit of C columns.
+__host__ __device__ inline int max_slice_cols(int R, int C, int S) {
+  int cb, ce;
+  slice_cols(C, R, 0, S, cb, ce);
+  return ce - cb;
 }
 
 __device__ __forceinline__ u32x4 lds_u32x4(uint32_t addr) {
@@ -294,14 +305,6 @@ __device__ __forceinline__ int lds_u16(uint32_t addr) {
 // hand data between its lanes through LDS (a wave's LDS operations are
 // executed in order, so no hardware wait is needed).
 __device__ __forceinline__ void lds_phase() { __asm__ __volatile__("" ::: "memory"); }
-
-// Group columns [cb, ce) of unit u owned by `wave`.
-__device__ __forceinline__ void wave_slice(const UnitInfo& u, int R, int wave, int& cb, int& ce) {
-  const int cw = cols_per_word(R);
-  const int per = ((u.cols + cw - 1) / cw + kWaves - 1) / kWaves;
-  cb = min(u.cols, wave * per * cw);
-  ce = min(u.cols, (wave + 1) * per * cw);
-}
 
 __device__ __forceinline__ uint64_t read_lane64(uint64_t v, int l) {
   const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, l), hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), l);
@@ -328,10 +331,24 @@ __device__ __forceinline__ WmapRegs load_wmap(const DevMatrix& mat, const UnitIn
   return r;
 }
 
+// Cross-lane moves on the VALU (DPP), no LDS round trip.  A lane whose
+// source is outside its row of 16 reads 0.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xf, 0xf, true);
+}
+constexpr int kDppShr1 = 0x111, kDppShr2 = 0x112, kDppShr4 = 0x114, kDppShr8 = 0x118;
+constexpr int kDppQuadXor1 = 0xB1, kDppQuadXor2 = 0x4E;  // quad_perm [1,0,3,2] and [2,3,0,1]
+
+// Sum over the wave (integers): prefix sums inside each row of 16 lanes,
+// then the four row totals.  The result is wave-uniform.
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
-  return v;
+  v += dpp<kDppShr1>(v);
+  v += dpp<kDppShr2>(v);
+  v += dpp<kDppShr4>(v);
+  v += dpp<kDppShr8>(v);
+  return __builtin_amdgcn_readlane(v, 15) + __builtin_amdgcn_readlane(v, 31) + __builtin_amdgcn_readlane(v, 47) +
+         __builtin_amdgcn_readlane(v, 63);
 }
 
 // Class counts of words [0, wb) of the unit (where the window's runs start
@@ -364,14 +381,14 @@ __device__ __forceinline__ WinCounts window_counts(const WmapRegs& wr, const Uni
   own01 = wave_sum(own01);
   own23 = wave_sum(own23);
   WinCounts wc;
-  wc.before[0] = uniform(bef01 & 0xFFFF);
-  wc.before[1] = uniform(bef01 >> 16);
-  wc.before[2] = uniform(bef23 & 0xFFFF);
-  wc.before[3] = uniform(bef23 >> 16);
-  wc.own[0] = uniform(own01 & 0xFFFF);
-  wc.own[1] = uniform(own01 >> 16);
-  wc.own[2] = uniform(own23 & 0xFFFF);
-  wc.own[3] = uniform(own23 >> 16);
+  wc.before[0] = bef01 & 0xFFFF;
+  wc.before[1] = bef01 >> 16;
+  wc.before[2] = bef23 & 0xFFFF;
+  wc.before[3] = bef23 >> 16;
+  wc.own[0] = own01 & 0xFFFF;
+  wc.own[1] = own01 >> 16;
+  wc.own[2] = own23 & 0xFFFF;
+  wc.own[3] = own23 >> 16;
   return wc;
 }
 
@@ -422,19 +439,23 @@ struct Batch {
   uint16_t s[E];
 };
 
-// Every lane always loads: lanes past the end re-read the last entry of the
-// run.  Unconditional loads keep the number of outstanding loads the same on
-// every path, so the compiler waits only for the batch it is about to decode
-// and the next batch stays in flight (a conditional load makes it wait for all).
+// Every lane always loads, whatever the run's length (lanes past the end
+// re-read its last entry, clamped into the class section, and an empty run
+// reads the section's first entry or, for an empty class, the unit table).
+// Unconditional loads keep the number of outstanding loads the same on every
+// path, so the compiler waits only for the batch it is about to decode and
+// later batches stay in flight (a conditional load makes it wait for all).
 template <int CLS>
-__device__ __forceinline__ void load_batch(Batch<CLS>& bt, const uint32_t* __restrict__ codes,
-                                           const uint16_t* __restrict__ scales, uint32_t start, int n, int b,
+__device__ __forceinline__ void load_batch(Batch<CLS>& bt, const DevMatrix& mat, uint32_t start, int n, int b,
                                            uint32_t lane) {
   constexpr int NW = Batch<CLS>::NW, E = Batch<CLS>::E;
+  const uint32_t* __restrict__ codes = (const uint32_t*)mat.codes[CLS];
+  const uint16_t* __restrict__ scales = mat.scales[CLS];
+  const uint32_t lim = mat.last_entry[CLS];
 #pragma unroll
   for (int i = 0; i < E; ++i) {
-    const int e = min((b * E + i) * 64 + (int)lane, n - 1);
-    const size_t g = (size_t)start + (uint32_t)e;
+    const int e = max(min((b * E + i) * 64 + (int)lane, n - 1), 0);
+    const size_t g = min(start + (uint32_t)e, lim);
     bt.s[i] = scales[g];
     if constexpr (NW == 2) {
       const u32x2 v = __builtin_nontemporal_load((const u32x2*)(codes + g * NW));
@@ -511,7 +532,8 @@ __device__ __forceinline__ void decode_batch(const Batch<CLS>& bt, uint32_t inv_
   constexpr int NW = Batch<CLS>::NW, E = Batch<CLS>::E;
   int p[E];
 #pragma unroll
-  for (int i = 0; i < E; ++i) p[i] = lds_u16(inv_c + 2u * (uint32_t)min((b * E + i) * 64 + (int)lane, n - 1));
+  for (int i = 0; i < E; ++i)
+    p[i] = lds_u16(inv_c + 2u * (uint32_t)max(min((b * E + i) * 64 + (int)lane, n - 1), 0));
 #pragma unroll
   for (int i = 0; i < E; ++i) {
     const int g0 = (b * E + i) * 64;
@@ -522,24 +544,22 @@ __device__ __forceinline__ void decode_batch(const Batch<CLS>& bt, uint32_t inv_
 }
 
 // The n entries of class CLS of the window, starting at entry `start` of the
-// class section; the next batch is in flight while the current one is
-// decoded (past the last batch the load repeats the last batch, which keeps
-// the loop free of conditional loads).  If `have`, batch 0 is already in A.
+// class section.  Batch 0 is already in A (loaded with the other classes'
+// first batches); the next batch is in flight while the current one is
+// decoded.  The loop runs at least once and its loads are unconditional
+// (past the last batch they repeat it), so the count of outstanding loads
+// never depends on the data.
 template <int CLS, int MT>
-__device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS>& A, bool have, uint32_t start, int n,
+__device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS>& A, uint32_t start, int n,
                                           uint32_t inv_c, const Win& wn, uint32_t lane) {
-  if (n <= 0) return;
-  const uint32_t* codes = (const uint32_t*)mat.codes[CLS];
-  const uint16_t* scales = mat.scales[CLS];
   constexpr int per_batch = Batch<CLS>::E * 64;
-  const int nb = (n + per_batch - 1) / per_batch;
-  if (!have) load_batch<CLS>(A, codes, scales, start, n, 0, lane);
+  const int nb = max(1, (n + per_batch - 1) / per_batch);
   Batch<CLS> B;
   for (int b = 0; b < nb; b += 2) {
-    load_batch<CLS>(B, codes, scales, start, n, min(b + 1, nb - 1), lane);
+    load_batch<CLS>(B, mat, start, n, min(b + 1, nb - 1), lane);
     decode_batch<CLS, MT>(A, inv_c, n, b, lane, wn);
     if (b + 1 >= nb) break;
-    load_batch<CLS>(A, codes, scales, start, n, min(b + 2, nb - 1), lane);
+    load_batch<CLS>(A, mat, start, n, min(b + 2, nb - 1), lane);
     decode_batch<CLS, MT>(B, inv_c, n, b + 1, lane, wn);
   }
 }
@@ -554,14 +574,25 @@ __device__ __forceinline__ void load_x1(const uint16_t* __restrict__ x, int j, i
   const int n = cols * 8;
 #pragma unroll
   for (int k = 0; k < kXRegs; ++k) {
-    const int i = min((int)lane + 64 * k, n - 1);
+    const int i = max(min((int)lane + 64 * k, n - 1), 0);
     xr.v[k] = *(const u32x4*)(x + (size_t)(j + (i >> 3)) * 64 + (i & 7) * 8);
   }
 }
 
 // Stores the chunks to LDS and writes each column's activation sum: every
-// lane sums its chunk, then the 8 lanes of a column combine their sums with
-// a fixed butterfly (the same value in all 8 lanes).
+// lane sums its chunk, the lanes of each quad add their sums pairwise
+// (xor 1, then xor 2), and the last lane of the column's eight adds the
+// first quad's sum to its own (a fixed order).
+__device__ __forceinline__ float add_dpp_f32_quad_xor1(float s) {
+  return s + __builtin_bit_cast(float, dpp<kDppQuadXor1>(__builtin_bit_cast(uint32_t, s)));
+}
+__device__ __forceinline__ float add_dpp_f32_quad_xor2(float s) {
+  return s + __builtin_bit_cast(float, dpp<kDppQuadXor2>(__builtin_bit_cast(uint32_t, s)));
+}
+__device__ __forceinline__ float add_dpp_f32_shr4(float s) {
+  return s + __builtin_bit_cast(float, dpp<kDppShr4>(__builtin_bit_cast(uint32_t, s)));
+}
+
 __device__ __forceinline__ void store_x1(int cols, const XRegs& xr, const Win& wn, uint32_t lane) {
   const int n = cols * 8;
   const uint32_t ones = 0x3C003C00u;  // (1.0, 1.0)
@@ -574,12 +605,10 @@ __device__ __forceinline__ void store_x1(int cols, const XRegs& xr, const Win& w
       sum = dot2(v.y, ones, sum);
       sum = dot2(v.z, ones, sum);
       sum = dot2(v.w, ones, sum);
-      sum += __shfl_xor(sum, 1, 64);
-      sum += __shfl_xor(sum, 2, 64);
-      sum += __shfl_xor(sum, 4, 64);
+      sum = add_dpp_f32_shr4(add_dpp_f32_quad_xor2(add_dpp_f32_quad_xor1(sum)));
       if (i < n) {
         lds_store_u32x4(wn.xs + (uint32_t)((i >> 3) * kXStride + (i & 7) * 16), v);
-        if ((i & 7) == 0) lds_store_f32(wn.Xs + 4u * (uint32_t)(i >> 3), sum);
+        if ((i & 7) == 7) lds_store_f32(wn.Xs + 4u * (uint32_t)(i >> 3), sum);
       }
     }
   }
@@ -650,11 +679,14 @@ __device__ __forceinline__ int clamp_run(const DevMatrix& mat, int c, uint32_t s
   return start >= lim ? 0 : (int)min(n, lim - start);
 }
 
-template <int MT>
-__global__ __launch_bounds__(kThreads, MT == 1 ? VBQ_MV_WAVES_PER_SIMD : 2) void vbq_mv_kernel(MvArgs a) {
+// One activation row keeps 4 waves per SIMD (at most 128 VGPRs); more rows
+// trade occupancy for registers.
+template <int MT, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 4 : 2))) void vbq_mv_kernel(
+    MvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const DevMatrix& mat = a.m;
-  const int R = mat.R, SW = a.SW;
+  const int R = mat.R, SW = a.SW, S = a.S;
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
   const uint32_t lane = lane_id();
   const int wave = wave_id();
@@ -662,7 +694,7 @@ __global__ __launch_bounds__(kThreads, MT == 1 ? VBQ_MV_WAVES_PER_SIMD : 2) void
   const int NS = MT * R;
   const WavePlan P = wave_plan(R, SW, MT);
   const uint32_t ysum = lds0 + (uint32_t)(wave * NS * 4);
-  const uint32_t region = lds0 + (uint32_t)(kWaves * NS * 4 + wave * P.bytes);
+  const uint32_t region = lds0 + (uint32_t)(NW * NS * 4 + wave * P.bytes);
   Win wn;
   wn.xs = region + P.xs;
   wn.Xs = region + P.Xs;
@@ -674,18 +706,19 @@ __global__ __launch_bounds__(kThreads, MT == 1 ? VBQ_MV_WAVES_PER_SIMD : 2) void
   const uint32_t inv = region + P.inv;
   for (int i = (int)lane; i < NS; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
 
-  for (int k = 0; k < mat.U; ++k) {
+  for (int item = wave; item < mat.U * S; item += NW) {
+    const int k = item / S, sl = item - k * S;
     const UnitInfo u = load_unit(mat, t, k);
     const int unit = t * mat.U + k;
     int cb, ce;
-    wave_slice(u, R, wave, cb, ce);
-    if (cb >= ce) continue;  // wave-uniform: this wave has no columns here
+    slice_cols(u.cols, R, sl, S, cb, ce);
+    if (cb >= ce) continue;  // wave-uniform: an empty slice
     const int slice_we = (ce * R + 63) >> 6;
     uint32_t ustart[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) ustart[c] = class_start(mat, unit, c);
     XRegs xr;
-    if constexpr (MT == 1) load_x1(a.x, u.j0 + cb, ce - cb, xr, lane);  // before the map: one latency
+    if constexpr (MT == 1) load_x1(a.x, u.j0 + cb, ce - cb, xr, lane);  // with the map: one latency
     const WmapRegs wr = load_wmap(mat, u, slice_we, lane);
     auto window = [&](int c0, int c1) __attribute__((always_inline)) {
       const int cols = c1 - c0;
@@ -701,20 +734,27 @@ __global__ __launch_bounds__(kThreads, MT == 1 ? VBQ_MV_WAVES_PER_SIMD : 2) void
         seg[c] = inv + 2u * o;
         o += wc.own[c];
       }
-      // the first batch of 1-bit codes is in flight while x is staged and the index built
+      // the first batches of the 1-, 2- and 4-bit classes are in flight while
+      // the index is built and x is staged (the 8-bit one, twice as wide,
+      // would not fit the register budget and is loaded when its turn comes)
       Batch<0> A0;
-      const bool have0 = n[0] > 0;
-      if (have0) load_batch<0>(A0, (const uint32_t*)mat.codes[0], mat.scales[0], start[0], n[0], 0, lane);
+      Batch<1> A1;
+      Batch<2> A2;
+      Batch<3> A3;
+      load_batch<0>(A0, mat, start[0], n[0], 0, lane);
+      load_batch<1>(A1, mat, start[1], n[1], 0, lane);
+      load_batch<2>(A2, mat, start[2], n[2], 0, lane);
       build_index(wr, u, wb, we, R, wc, inv, lane);
       if constexpr (MT == 1)
         store_x1(cols, xr, wn, lane);
       else
         stage_x<MT>(a, u.j0 + c0, cols, wn, lane);
       lds_phase();
-      run_class<0, MT>(mat, A0, have0, start[0], n[0], seg[0], wn, lane);
-      { Batch<1> A; run_class<1, MT>(mat, A, false, start[1], n[1], seg[1], wn, lane); }
-      { Batch<2> A; run_class<2, MT>(mat, A, false, start[2], n[2], seg[2], wn, lane); }
-      { Batch<3> A; run_class<3, MT>(mat, A, false, start[3], n[3], seg[3], wn, lane); }
+      run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
+      run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
+      run_class<2, MT>(mat, A2, start[2], n[2], seg[2], wn, lane);
+      load_batch<3>(A3, mat, start[3], n[3], 0, lane);
+      run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
       lds_phase();
       reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
       lds_phase();
@@ -727,20 +767,23 @@ __global__ __launch_bounds__(kThreads, MT == 1 ? VBQ_MV_WAVES_PER_SIMD : 2) void
   }
   __syncthreads();
   const int rows = min(R, mat.N - t * R);
-  for (int slot = threadIdx.x; slot < NS; slot += kThreads) {
+  for (int slot = threadIdx.x; slot < NS; slot += NW * 64) {
     const int m = slot >> mat.logR, r = slot & (R - 1);
     if (m < a.M && r < rows) {
       float tot = 0.0f;
 #pragma unroll
-      for (int w2 = 0; w2 < kWaves; ++w2) tot += lds_f32(lds0 + 4u * (uint32_t)(w2 * NS + slot));
+      for (int w2 = 0; w2 < NW; ++w2) tot += lds_f32(lds0 + 4u * (uint32_t)(w2 * NS + slot));
       a.y[m * a.ldy + (size_t)t * R + r] = tot;
     }
   }
 }
 
-// w_hat = s*q written densely (checking aid, not a hot path): each wave
-// indexes its slice (one window) and writes its entries, one lane per entry.
-__global__ __launch_bounds__(kThreads) void vbq_dequant_kernel(DevMatrix mat, float* W, int region_bytes) {
+// w_hat = s*q written densely (checking aid, not a hot path): four waves per
+// tile, each indexing slice `wave` of every unit (one window) and writing its
+// entries, one lane per entry.
+constexpr int kDequantWaves = 4;
+
+__global__ __launch_bounds__(kDequantWaves * 64) void vbq_dequant_kernel(DevMatrix mat, float* W, int region_bytes) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const uint32_t lane = lane_id();
   const int wave = wave_id();
@@ -751,7 +794,7 @@ __global__ __launch_bounds__(kThreads) void vbq_dequant_kernel(DevMatrix mat, fl
     const UnitInfo u = load_unit(mat, t, k);
     const int unit = t * mat.U + k;
     int cb, ce;
-    wave_slice(u, R, wave, cb, ce);
+    slice_cols(u.cols, R, wave, kDequantWaves, cb, ce);
     if (cb >= ce) continue;
     const int wb = (cb * R) >> 6, we = (ce * R + 63) >> 6;
     const WmapRegs wr = load_wmap(mat, u, we, lane);
@@ -760,7 +803,7 @@ __global__ __launch_bounds__(kThreads) void vbq_dequant_kernel(DevMatrix mat, fl
     lds_phase();
     uint32_t seg = inv;
     for (int c = 0; c < 4; ++c) {
-      const int B = 1 << c, NW = 2 * B, per = 16 / B;
+      const int B = 1 << c, NWc = 2 * B, per = 16 / B;
       const uint32_t mask = (1u << B) - 1;
       const uint32_t start = class_start(mat, unit, c) + wc.before[c];
       const int n = clamp_run(mat, c, start, wc.own[c]);
@@ -768,7 +811,7 @@ __global__ __launch_bounds__(kThreads) void vbq_dequant_kernel(DevMatrix mat, fl
         const int p = lds_u16(seg + 2u * (uint32_t)e) + wb * 64;  // unit position
         const int jl = p >> mat.logR, r = p & (R - 1);
         const size_t g = (size_t)start + e;
-        const uint32_t* wv = (const uint32_t*)mat.codes[c] + g * NW;
+        const uint32_t* wv = (const uint32_t*)mat.codes[c] + g * NWc;
         const float s = (float)__builtin_bit_cast(_Float16, mat.scales[c][g]);
         float* dst = W + ((size_t)t * R + r) * mat.K + (size_t)(u.j0 + jl) * 64;
         for (int i = 0; i < 32; ++i) {
@@ -808,8 +851,24 @@ vbq_status make_dev_matrix(const vbq_desc* d, const void* blob, DevMatrix* m) {
     m->scales[c] = (const uint16_t*)(b + d->section_off[VBQ_SEC_SCALES0 + c]);
     m->n_entries[c] = (uint32_t)d->n_entries[c];
   }
+  for (int c = 0; c < 4; ++c) {
+    if (m->n_entries[c] == 0) {  // loads of an empty class are clamped to the unit table
+      m->codes[c] = b;
+      m->scales[c] = (const uint16_t*)b;
+      m->last_entry[c] = 0;
+    } else {
+      m->last_entry[c] = m->n_entries[c] - 1;
+    }
+  }
   m->wmap_words = (uint32_t)(d->section_len[VBQ_SEC_WMAP] / 8);
   if (m->wmap_words == 0) return VBQ_ERR_DESC;
+  {
+    const int64_t G = d->K / 64, C = d->chunk_groups, R = d->tile_rows, U = d->n_chunks;
+    const int64_t wf = (C * R + 63) / 64, wl = ((G - (U - 1) * C) * R + 63) / 64;
+    m->chunk_words = (uint32_t)wf;
+    m->tile_words = (uint32_t)(2 * ((U - 1) * wf + wl));
+    if ((uint64_t)m->tile_words * (uint64_t)d->n_tiles != m->wmap_words) return VBQ_ERR_DESC;
+  }
   m->N = (int32_t)d->N;
   m->K = (int32_t)d->K;
   m->G = (int32_t)(d->K / 64);
@@ -824,26 +883,84 @@ vbq_status make_dev_matrix(const vbq_desc* d, const void* blob, DevMatrix* m) {
 }
 
 constexpr int kLdsLimit = 160 * 1024;
+constexpr int kMinWaves = 4;
 
-// Window columns for MT activation rows: the whole wave slice if it fits the
-// LDS budget (64 KB, else the 160 KB of a CU), else the largest multiple of
-// the columns per width-map word that does.  One row keeps x of a window in
-// registers and always takes the whole slice (at most 32 columns, since
-// C <= 128 and a slice is a quarter of the unit rounded up to whole words).
-int choose_window(int R, int C, int MT) {
-  const int cw = cols_per_word(R);
-  const int full = max_slice_cols(R, C);
-  if (MT == 1) return full <= kXRegs * 8 && mv_lds_bytes(R, full, 1) <= kLdsLimit ? full : 0;
-  for (int limit : {64 * 1024, kLdsLimit}) {
-    if (mv_lds_bytes(R, full, MT) <= limit) return full;
-    for (int sw = (full / cw) * cw; sw >= cw; sw -= cw)
-      if (mv_lds_bytes(R, sw, MT) <= limit) return sw;
+// Launch shape of the fused product for MT activation rows.
+struct MvShape {
+  int NW;  // waves per workgroup (4, 8 or 16)
+  int S;   // slices per unit
+  int SW;  // window columns
+  int lds; // dynamic LDS bytes
+};
+
+// Slices per unit: enough for four per tile, and for one activation row
+// narrow enough for the window to be the whole slice (at most 32 columns of
+// x held in registers).  Waves per workgroup: one per (unit, slice) item, as
+// a power of two from 4 to 16 (8 for several rows), so that a wave's items
+// (a chain of dependent loads each) run side by side rather than in turn.
+// Window: the whole slice if it fits the LDS budget (64 KB, else the 160 KB
+// of a CU), else the largest multiple of the columns per width-map word
+// that does.
+bool choose_shape(const DevMatrix& m, int MT, MvShape* sh) {
+  int S = (kMinWaves + m.U - 1) / m.U;
+  if (MT == 1)
+    while (max_slice_cols(m.R, m.C, S) > kXRegs * 8) ++S;
+  const int max_nw = MT == 1 ? 16 : 8;  // several rows need more than 128 VGPRs: 2 waves per SIMD
+  int NW = kMinWaves;
+  while (NW < max_nw && NW < m.U * S) NW *= 2;
+  const int cw = cols_per_word(m.R);
+  const int full = max_slice_cols(m.R, m.C, S);
+  int SW = 0;
+  if (MT == 1) {
+    if (mv_lds_bytes(m.R, full, 1, NW) <= kLdsLimit) SW = full;
+  } else {
+    for (int limit : {64 * 1024, kLdsLimit}) {
+      if (mv_lds_bytes(m.R, full, MT, NW) <= limit) {
+        SW = full;
+        break;
+      }
+      for (int sw = (full / cw) * cw; sw >= cw && !SW; sw -= cw)
+        if (mv_lds_bytes(m.R, sw, MT, NW) <= limit) SW = sw;
+      if (SW) break;
+    }
   }
-  return 0;
+  if (SW <= 0) return false;
+  sh->NW = NW;
+  sh->S = S;
+  sh->SW = SW;
+  sh->lds = mv_lds_bytes(m.R, SW, MT, NW);
+  return true;
+}
+
+// Raises a kernel's dynamic LDS limit once per device.
+vbq_status allow_big_lds(const void* kernel, std::atomic<uint64_t>& done) {
+  int dev = 0;
+  vbq_status st = hip_status(hipGetDevice(&dev));
+  if (st != VBQ_OK) return st;
+  const uint64_t bit = 1ull << (dev & 63);
+  if (done.load(std::memory_order_acquire) & bit) return VBQ_OK;
+  st = hip_status(hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit));
+  if (st == VBQ_OK) done.fetch_or(bit, std::memory_order_release);
+  return st;
+}
+
+template <int MT, int NW>
+vbq_status launch_mv_nw(const MvArgs& a, int lds, hipStream_t s) {
+  const void* kernel = (const void*)vbq_mv_kernel<MT, NW>;
+  if (lds > 64 * 1024) {  // beyond the default dynamic LDS limit
+    static std::atomic<uint64_t> done{0};
+    vbq_status st = allow_big_lds(kernel, done);
+    if (st != VBQ_OK) return st;
+  }
+  MvArgs args = a;
+  void* kargs[] = {&args};
+  return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
 }
 
 template <int MT>
 vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, float* y, int64_t ldy, hipStream_t s) {
+  MvShape sh;
+  if (!choose_shape(m, MT, &sh)) return VBQ_ERR_UNSUPPORTED;
   MvArgs a;
   a.m = m;
   a.x = (const uint16_t*)x;
@@ -851,25 +968,13 @@ vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
   a.ldx = ldx;
   a.ldy = ldy;
   a.M = M;
-  a.SW = choose_window(m.R, m.C, MT);
-  if (a.SW <= 0) return VBQ_ERR_UNSUPPORTED;
-  const int lds = mv_lds_bytes(m.R, a.SW, MT);
-  if (lds > 64 * 1024) {  // beyond the default dynamic LDS limit: raise it once per device
-    static std::atomic<uint64_t> attr_set{0};
-    int dev = 0;
-    vbq_status st = hip_status(hipGetDevice(&dev));
-    if (st != VBQ_OK) return st;
-    const uint64_t bit = 1ull << (dev & 63);
-    if (!(attr_set.load(std::memory_order_acquire) & bit)) {
-      st = hip_status(
-          hipFuncSetAttribute((const void*)vbq_mv_kernel<MT>, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit));
-      if (st != VBQ_OK) return st;
-      attr_set.fetch_or(bit, std::memory_order_release);
-    }
+  a.S = sh.S;
+  a.SW = sh.SW;
+  if (sh.NW == 4) return launch_mv_nw<MT, 4>(a, sh.lds, s);
+  if constexpr (MT == 1) {
+    if (sh.NW == 16) return launch_mv_nw<MT, 16>(a, sh.lds, s);
   }
-  void* kargs[] = {&a};
-  return hip_status(
-      hipLaunchKernel((const void*)vbq_mv_kernel<MT>, dim3((unsigned)m.T), dim3(kThreads), kargs, (size_t)lds, s));
+  return launch_mv_nw<MT, 8>(a, sh.lds, s);
 }
 
 }  // namespace
@@ -913,12 +1018,10 @@ vbq_status vbq_dequant(const vbq_desc* desc, const void* blob_dev, float* W_dev,
   if (st != VBQ_OK) return st;
   if ((uintptr_t)W_dev % 4) return VBQ_ERR_BUFFER;
   // one uint16 per position of the widest wave slice, rounded up to whole words
-  const int cw = cols_per_word(m.R);
-  const int slice = ((max_slice_cols(m.R, m.C) + cw - 1) / cw) * cw;
-  int region = align16(((slice * m.R + 63) / 64) * 64 * 2);
+  int region = align16(((max_slice_cols(m.R, m.C, kDequantWaves) * m.R + 63) / 64) * 64 * 2);
   void* args[] = {&m, &W_dev, &region};
-  const int lds = kWaves * region;
-  return hip_status(hipLaunchKernel((const void*)vbq_dequant_kernel, dim3((unsigned)m.T), dim3(kThreads), args,
+  const int lds = kDequantWaves * region;
+  return hip_status(hipLaunchKernel((const void*)vbq_dequant_kernel, dim3((unsigned)m.T), dim3(kDequantWaves * 64), args,
                                     (size_t)lds, (hipStream_t)stream));
 }
 
