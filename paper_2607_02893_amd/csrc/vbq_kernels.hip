@@ -393,9 +393,38 @@ __device__ __forceinline__ WinCounts window_counts(const WmapRegs& wr, const Uni
 }
 
 // inv[k] (uint16, from byte offset `inv`) = window-local position of the
-// k-th entry of the window, entries ordered by class, then by position.  A
-// word's masks are read into scalar registers, each class's lanes are
-// enabled straight from its mask (inverse ballot) and mbcnt gives the rank.
+// k-th entry of the window, entries ordered by class, then by position.  One
+// pass per width-map word, lane l taking position 64w + l: its rank inside
+// its class is a masked bit count (mbcnt) of the class mask, its class
+// selects among the four candidate slots (lane masks used directly as select
+// conditions), and real positions write their slot.  No branch depends on
+// the data.  Words whose 64 positions are all real (every word but a unit's
+// last one, outside the ragged last tile) skip the validity masks.
+template <bool kFull>
+__device__ __forceinline__ void index_word(uint64_t p0, uint64_t p1, uint64_t valid, uint32_t pos, uint32_t run[4],
+                                           uint32_t inv) {
+  uint64_t m[4];
+  if constexpr (kFull) {
+    m[0] = ~(p0 | p1);
+    m[1] = p0 & ~p1;
+    m[2] = p1 & ~p0;
+    m[3] = p0 & p1;
+  } else {
+    class_masks(p0, p1, valid, m);
+  }
+  uint32_t slot[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    slot[c] = __builtin_amdgcn_mbcnt_hi((uint32_t)(m[c] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m[c], run[c]));
+  uint32_t k = slot[3];
+  k = __builtin_amdgcn_inverse_ballot_w64(m[2]) ? slot[2] : k;
+  k = __builtin_amdgcn_inverse_ballot_w64(m[1]) ? slot[1] : k;
+  k = __builtin_amdgcn_inverse_ballot_w64(m[0]) ? slot[0] : k;
+  if (kFull || __builtin_amdgcn_inverse_ballot_w64(valid)) lds_store_u16(inv + 2u * k, (uint16_t)pos);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) run[c] += (uint32_t)__popcll(m[c]);
+}
+
 __device__ __forceinline__ void build_index(const WmapRegs& wr, const UnitInfo& u, int wb, int we, int R,
                                             const WinCounts& wc, uint32_t inv, uint32_t lane) {
   uint32_t run[4];
@@ -403,22 +432,17 @@ __device__ __forceinline__ void build_index(const WmapRegs& wr, const UnitInfo& 
   run[1] = wc.own[0];
   run[2] = run[1] + wc.own[1];
   run[3] = run[2] + wc.own[2];
-  for (int w = wb; w < we; ++w) {
+  const int full_end = u.rows == R ? max(wb, min(we, u.npos >> 6)) : wb;
+  const uint32_t pos0 = lane - (uint32_t)wb * 64u;
+  // words held in lanes w (planes a0/a1) and w - 64 (planes b0/b1)
+  for (int w = wb; w < min(full_end, 64); ++w)
+    index_word<true>(read_lane64(wr.a0, w), read_lane64(wr.a1, w), ~0ull, pos0 + 64u * w, run, inv);
+  for (int w = max(wb, 64); w < full_end; ++w)
+    index_word<true>(read_lane64(wr.b0, w - 64), read_lane64(wr.b1, w - 64), ~0ull, pos0 + 64u * w, run, inv);
+  for (int w = full_end; w < we; ++w) {
     const bool hi = w >= 64;
-    const uint64_t p0 = read_lane64(hi ? wr.b0 : wr.a0, w & 63), p1 = read_lane64(hi ? wr.b1 : wr.a1, w & 63);
-    uint64_t m[4];
-    class_masks(p0, p1, valid_mask(w, u.npos, R, u.rows), m);
-    const uint16_t pos = (uint16_t)((w - wb) * 64 + (int)lane);
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      if (m[c]) {
-        if (__builtin_amdgcn_inverse_ballot_w64(m[c]))
-          lds_store_u16(inv + 2u * __builtin_amdgcn_mbcnt_hi((uint32_t)(m[c] >> 32),
-                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)m[c], run[c])),
-                        pos);
-        run[c] += (uint32_t)__popcll(m[c]);
-      }
-    }
+    index_word<false>(read_lane64(hi ? wr.b0 : wr.a0, w & 63), read_lane64(hi ? wr.b1 : wr.a1, w & 63),
+                      valid_mask(w, u.npos, R, u.rows), pos0 + 64u * w, run, inv);
   }
 }
 
