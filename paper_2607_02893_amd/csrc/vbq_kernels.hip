@@ -70,6 +70,14 @@ __device__ __forceinline__ float dot2(uint32_t codes, uint32_t xpair, float acc)
   return __builtin_amdgcn_fdot2(as_h2(codes), as_h2(xpair), acc, false);
 }
 
+// dot2 into a fresh accumulator: the three-operand form with an inline zero
+// (the accumulating two-operand form would need a register set to zero first)
+__device__ __forceinline__ float dot2_first(uint32_t codes, uint32_t xpair) {
+  float r;
+  __asm__("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(r) : "v"(codes), "v"(xpair));
+  return r;
+}
+
 __device__ __forceinline__ uint32_t shl(uint32_t w, int s) { return s >= 0 ? (w << s) : (w >> (-s)); }
 
 // ---------------------------------------------------------------------------
@@ -505,20 +513,24 @@ struct Win {  // LDS byte addresses of the wave's window buffers
   int SW, logR;        // window columns (Xs row stride), log2 R
 };
 
+// First pair index (0..31) whose field lands in accumulator slot `sl`.
+template <typename D>
+__device__ constexpr int first_pair_of_slot(int sl) {
+  for (int i = 0; i < 32; ++i)
+    if (D::slot(D::field(i % D::kFields).t) == sl) return i;
+  return 32;
+}
+
 // Decode one entry (64 weights) at window-local position p, reading the
 // activations of the MT rows from LDS chunk by chunk, and write its partial
-// product(s) to LDS (only lanes with `valid`).
+// product(s) to LDS.  Lanes past the end of a run hold a copy of the run's
+// last entry (clamped loads), so they store the same value to the same place.
 template <int CLS, int MT>
-__device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits, int p, bool valid,
-                                              const Win& wn) {
+__device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits, int p, bool valid, const Win& wn) {
   using D = DecFor<CLS, MT>;
   const int js = p >> wn.logR;
   const uint32_t xaddr = wn.xs + (uint32_t)__umul24((uint32_t)js, kXStride);
   float acc[MT][D::kSlots];
-#pragma unroll
-  for (int m = 0; m < MT; ++m)
-#pragma unroll
-    for (int k = 0; k < D::kSlots; ++k) acc[m][k] = 0.0f;
 #pragma unroll
   for (int q = 0; q < 8; ++q) {  // x chunk q holds pairs 4q..4q+3
     u32x4 xv[MT];
@@ -534,7 +546,12 @@ __device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits
       const uint32_t v = shl(w[wi], fd.shift) & mask;
       const int sl = D::slot(fd.t);
 #pragma unroll
-      for (int m = 0; m < MT; ++m) acc[m][sl] = dot2(v, xv[m][c4], acc[m][sl]);
+      for (int m = 0; m < MT; ++m) {
+        if (i == first_pair_of_slot<D>(sl))  // resolved at compile time
+          acc[m][sl] = MT <= 2 ? dot2_first(v, xv[m][c4]) : dot2(v, xv[m][c4], 0.0f);
+        else
+          acc[m][sl] = dot2(v, xv[m][c4], acc[m][sl]);
+      }
     }
   }
   const float s = (float)__builtin_bit_cast(_Float16, s_bits);
@@ -546,7 +563,9 @@ __device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits
     for (int k = 1; k < D::kSlots; ++k) su = __builtin_fmaf(acc[m][k], D::inv_value(k), su);
     const float X = lds_f32(wn.Xs + 4u * (uint32_t)(m * wn.SW + js));
     const float sq = CLS == 0 ? __builtin_fmaf(su, 2.0f, -X) : __builtin_fmaf(-(float)(1 << (D::B - 1)), X, su);
-    if (valid) lds_store_f32(paddr + (uint32_t)m * wn.part_m, s * sq);
+    // (several rows: skipping the duplicates keeps the register allocator's
+    // scheduling regions small; one row stores them, with no branch)
+    if (MT == 1 || valid) lds_store_f32(paddr + (uint32_t)m * wn.part_m, s * sq);
   }
 }
 
