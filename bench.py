@@ -171,6 +171,43 @@ def cpu_baseline(wl, budget_s=20.0):
             "gb_per_s_equiv": None}
 
 
+def write_traffic_file(path, summ):
+    """The committed form of the counter summary that measured_traffic() reads."""
+    lines = [
+        "# HBM traffic of vbq_mv_kernel<1>: 9B-class decode step (129 GEMVs, M=1)",
+        "",
+        "Two counter passes over `bench.py --profile --steps 2 --warmup 1` (3 steps x 129 launches),",
+        "then a plain copy of 256 MiB (torch.mul by 1.0) to scale the counters to bytes:",
+        "",
+        "```",
+        "cd /tmp && export TMPDIR=/tmp",
+        "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pmc_fetch -o run -- "
+        "python3 $R/bench.py --profile --steps 2 --warmup 1",
+        "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pmc_write -o run -- "
+        "python3 $R/bench.py --profile --steps 2 --warmup 1",
+        "python3 bench.py --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write --write-traffic <this file>",
+        "```",
+        "",
+        "(`$R` is the repository root.)  Per-launch figures, averaged over every GEMV launch of the step:",
+        "",
+        f"- launches: {summ['launches']}",
+        f"- fetch_kib_per_launch_raw: {summ['fetch_kib_per_launch_raw']:.1f}",
+        f"- write_kib_per_launch_raw: {summ['write_kib_per_launch_raw']:.1f}",
+        f"- copy_fetch_kib (256 MiB read): {summ['copy_fetch_kib']:.0f}",
+        f"- copy_write_kib (256 MiB written): {summ['copy_write_kib']:.0f}",
+        f"- fetch_scale: {summ['fetch_scale']:.4f}",
+        f"- write_scale: {summ['write_scale']:.4f}",
+        f"- fetch_bytes_per_launch: {summ['fetch_bytes_per_launch']:.0f}",
+        f"- write_bytes_per_launch: {summ['write_bytes_per_launch']:.0f}",
+        f"- hbm_bytes_per_launch: {summ['hbm_bytes_per_launch']}",
+        f"- kernel_source_sha256: `{summ['kernel_source_sha256']}`",
+        "",
+        "bench.py reports hbm_bytes_per_launch as roofline.traffic while the kernel source still has this hash.",
+    ]
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -183,9 +220,13 @@ def main():
     ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 (eager launches only)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs of --profile (FETCH_SIZE, WRITE_SIZE) and exit")
+    ap.add_argument("--write-traffic", metavar="PATH", help="with --pmc-summary: write the traffic summary file")
     args = ap.parse_args()
     if args.pmc_summary:
-        print(json.dumps(pmc_summary(*args.pmc_summary)), flush=True)
+        summ = pmc_summary(*args.pmc_summary)
+        print(json.dumps(summ), flush=True)
+        if args.write_traffic:
+            write_traffic_file(args.write_traffic, summ)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the fused GEMV path has no multi-GPU mode in this build "
