@@ -14,8 +14,10 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libvbq.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 ARCH = "gfx950"
-# packed fp32 instructions are kept out of every HIP kernel
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# packed fp32 instructions are kept out of every HIP kernel; the GEMV kernel's
+# eleven leading scalar arguments are preloaded into SGPRs
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-kernarg-preload-count=11"]
 
 
 def _run(cmd, verbose):

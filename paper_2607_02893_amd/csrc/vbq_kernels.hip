@@ -40,19 +40,28 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 
+// One packed matrix on the device.  Every section is addressed by a 32-bit
+// byte offset from the blob start (blobs are below 4 GiB), so loads use a
+// scalar 64-bit base with a 32-bit per-lane offset.
 struct DevMatrix {
-  const uint32_t* units;
-  const uint64_t* wmap;
-  const uint8_t* codes[4];
-  const uint16_t* scales[4];
+  const uint8_t* blob;
+  uint32_t off_units, off_wmap;
+  uint32_t off_codes[4], off_scales[4];  // an empty class points at the unit table (offset 0)
   uint32_t n_entries[4];
-  uint32_t last_entry[4];  // load clamp: n_entries - 1 (0 for an empty class, whose pointers then
-                           // name the unit table so that clamped loads stay inside the blob)
-  uint32_t wmap_words;     // 64-bit words in the width-map section
-  uint32_t tile_words;     // width-map words of one row tile (all its units, both planes)
-  uint32_t chunk_words;    // width-map words per plane of a unit with C columns
+  uint32_t wmap_words;   // 64-bit words in the width-map section
+  uint32_t tile_words;   // width-map words of one row tile (all its units, both planes)
+  uint32_t chunk_words;  // width-map words per plane of a unit with C columns
   int32_t N, K, G, R, C, T, U, logR;
 };
+
+template <typename T>
+__device__ __forceinline__ T ld(const uint8_t* base, uint32_t off) {
+  return *(const T*)(base + off);
+}
+template <typename T>
+__device__ __forceinline__ T ld_nt(const uint8_t* base, uint32_t off) {
+  return __builtin_nontemporal_load((const T*)(base + off));
+}
 
 struct MvArgs {
   DevMatrix m;
@@ -332,10 +341,10 @@ __device__ __forceinline__ WmapRegs load_wmap(const DevMatrix& mat, const UnitIn
   const uint32_t top = (uint32_t)(max(we, 1) - 1);
   const uint32_t wa = min(lane, top), wb = min(lane + 64u, top);
   WmapRegs r;
-  r.a0 = mat.wmap[min(u.wmap_word + wa, last)];
-  r.a1 = mat.wmap[min(u.wmap_word + (uint32_t)u.W + wa, last)];
-  r.b0 = mat.wmap[min(u.wmap_word + wb, last)];
-  r.b1 = mat.wmap[min(u.wmap_word + (uint32_t)u.W + wb, last)];
+  r.a0 = ld<uint64_t>(mat.blob, mat.off_wmap + 8u * min(u.wmap_word + wa, last));
+  r.a1 = ld<uint64_t>(mat.blob, mat.off_wmap + 8u * min(u.wmap_word + (uint32_t)u.W + wa, last));
+  r.b0 = ld<uint64_t>(mat.blob, mat.off_wmap + 8u * min(u.wmap_word + wb, last));
+  r.b1 = ld<uint64_t>(mat.blob, mat.off_wmap + 8u * min(u.wmap_word + (uint32_t)u.W + wb, last));
   return r;
 }
 
@@ -481,22 +490,21 @@ template <int CLS>
 __device__ __forceinline__ void load_batch(Batch<CLS>& bt, const DevMatrix& mat, uint32_t start, int n, int b,
                                            uint32_t lane) {
   constexpr int NW = Batch<CLS>::NW, E = Batch<CLS>::E;
-  const uint32_t* __restrict__ codes = (const uint32_t*)mat.codes[CLS];
-  const uint16_t* __restrict__ scales = mat.scales[CLS];
-  const uint32_t lim = mat.last_entry[CLS];
+  const uint32_t lim = max(mat.n_entries[CLS], 1u) - 1u;
 #pragma unroll
   for (int i = 0; i < E; ++i) {
     const int e = max(min((b * E + i) * 64 + (int)lane, n - 1), 0);
-    const size_t g = min(start + (uint32_t)e, lim);
-    bt.s[i] = scales[g];
+    const uint32_t g = min(start + (uint32_t)e, lim);
+    bt.s[i] = ld<uint16_t>(mat.blob, mat.off_scales[CLS] + 2u * g);
+    const uint32_t off = mat.off_codes[CLS] + g * (4u * NW);
     if constexpr (NW == 2) {
-      const u32x2 v = __builtin_nontemporal_load((const u32x2*)(codes + g * NW));
+      const u32x2 v = ld_nt<u32x2>(mat.blob, off);
       bt.w[2 * i] = v.x;
       bt.w[2 * i + 1] = v.y;
     } else {
 #pragma unroll
       for (int k = 0; k < NW / 4; ++k) {
-        const u32x4 v = __builtin_nontemporal_load((const u32x4*)(codes + g * NW) + k);
+        const u32x4 v = ld_nt<u32x4>(mat.blob, off + 16u * k);
         bt.w[i * NW + 4 * k] = v.x;
         bt.w[i * NW + 4 * k + 1] = v.y;
         bt.w[i * NW + 4 * k + 2] = v.z;
@@ -712,7 +720,7 @@ __device__ __forceinline__ void reduce_window(const Win& wn, int R, int cols, in
 
 // Start of unit `unit`'s class-c run in the class section.
 __device__ __forceinline__ uint32_t class_start(const DevMatrix& mat, int unit, int c) {
-  return mat.units[(size_t)unit * vbq::kUnitRowWords + c];
+  return ld<uint32_t>(mat.blob, mat.off_units + 4u * ((uint32_t)unit * vbq::kUnitRowWords + c));
 }
 
 // Entries of a run that stay inside the class section (a malformed blob can
@@ -724,12 +732,34 @@ __device__ __forceinline__ int clamp_run(const DevMatrix& mat, int c, uint32_t s
 
 // One activation row keeps 4 waves per SIMD (at most 128 VGPRs); more rows
 // trade occupancy for registers.
+//
+// The values the first memory accesses depend on come as separate leading
+// arguments, which the command processor can place in SGPRs before the wave
+// starts (kernel-argument preloading), so the first loads do not wait for a
+// kernel-argument fetch.  geo packs R (9 bits), C (8), log2 R (4) and S (8);
+// sw_m packs SW (16) and M (16).  (At most 16 SGPRs can be preloaded, two
+// of which hold the kernel-argument pointer: these eleven take 13.)
 template <int MT, int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 4 : 2))) void vbq_mv_kernel(
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ blob, uint32_t off_wmap, uint32_t tile_words,
+    uint32_t chunk_words, uint32_t wmap_words, int32_t G, int32_t N, uint32_t geo, int32_t U, uint32_t sw_m,
     MvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  const DevMatrix& mat = a.m;
-  const int R = mat.R, SW = a.SW, S = a.S;
+  DevMatrix mat = a.m;
+  mat.blob = blob;
+  mat.off_wmap = off_wmap;
+  mat.tile_words = tile_words;
+  mat.chunk_words = chunk_words;
+  mat.wmap_words = wmap_words;
+  mat.G = G;
+  mat.N = N;
+  mat.U = U;
+  mat.R = (int)(geo & 0x1FF);
+  mat.C = (int)((geo >> 9) & 0xFF);
+  mat.logR = (int)((geo >> 17) & 0xF);
+  a.x = x;
+  a.M = (int)(sw_m >> 16);
+  const int R = mat.R, SW = (int)(sw_m & 0xFFFF), S = (int)(geo >> 21);
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
   const uint32_t lane = lane_id();
   const int wave = wave_id();
@@ -854,8 +884,8 @@ __global__ __launch_bounds__(kDequantWaves * 64) void vbq_dequant_kernel(DevMatr
         const int p = lds_u16(seg + 2u * (uint32_t)e) + wb * 64;  // unit position
         const int jl = p >> mat.logR, r = p & (R - 1);
         const size_t g = (size_t)start + e;
-        const uint32_t* wv = (const uint32_t*)mat.codes[c] + g * NWc;
-        const float s = (float)__builtin_bit_cast(_Float16, mat.scales[c][g]);
+        const uint32_t* wv = (const uint32_t*)(mat.blob + mat.off_codes[c]) + g * NWc;
+        const float s = (float)__builtin_bit_cast(_Float16, ld<uint16_t>(mat.blob, mat.off_scales[c] + 2u * (uint32_t)g));
         float* dst = W + ((size_t)t * R + r) * mat.K + (size_t)(u.j0 + jl) * 64;
         for (int i = 0; i < 32; ++i) {
           const uint32_t word = wv[i / per];
@@ -886,22 +916,15 @@ vbq_status make_dev_matrix(const vbq_desc* d, const void* blob, DevMatrix* m) {
   vbq_status st = vbq_desc_check(d);
   if (st != VBQ_OK) return st;
   if ((uintptr_t)blob % 256 != 0) return VBQ_ERR_BUFFER;
-  const uint8_t* b = (const uint8_t*)blob;
-  m->units = (const uint32_t*)(b + d->section_off[VBQ_SEC_UNITS]);
-  m->wmap = (const uint64_t*)(b + d->section_off[VBQ_SEC_WMAP]);
+  if (d->total_bytes >= (1ull << 32)) return VBQ_ERR_UNSUPPORTED;  // 32-bit section offsets
+  m->blob = (const uint8_t*)blob;
+  m->off_units = (uint32_t)d->section_off[VBQ_SEC_UNITS];
+  m->off_wmap = (uint32_t)d->section_off[VBQ_SEC_WMAP];
   for (int c = 0; c < 4; ++c) {
-    m->codes[c] = b + d->section_off[VBQ_SEC_CODES0 + c];
-    m->scales[c] = (const uint16_t*)(b + d->section_off[VBQ_SEC_SCALES0 + c]);
     m->n_entries[c] = (uint32_t)d->n_entries[c];
-  }
-  for (int c = 0; c < 4; ++c) {
-    if (m->n_entries[c] == 0) {  // loads of an empty class are clamped to the unit table
-      m->codes[c] = b;
-      m->scales[c] = (const uint16_t*)b;
-      m->last_entry[c] = 0;
-    } else {
-      m->last_entry[c] = m->n_entries[c] - 1;
-    }
+    // loads of an empty class are clamped to the unit table's first bytes
+    m->off_codes[c] = m->n_entries[c] ? (uint32_t)d->section_off[VBQ_SEC_CODES0 + c] : m->off_units;
+    m->off_scales[c] = m->n_entries[c] ? (uint32_t)d->section_off[VBQ_SEC_SCALES0 + c] : m->off_units;
   }
   m->wmap_words = (uint32_t)(d->section_len[VBQ_SEC_WMAP] / 8);
   if (m->wmap_words == 0) return VBQ_ERR_DESC;
@@ -996,7 +1019,14 @@ vbq_status launch_mv_nw(const MvArgs& a, int lds, hipStream_t s) {
     if (st != VBQ_OK) return st;
   }
   MvArgs args = a;
-  void* kargs[] = {&args};
+  const uint16_t* x = a.x;
+  const uint8_t* blob = a.m.blob;
+  uint32_t off_wmap = a.m.off_wmap, tile_words = a.m.tile_words, chunk_words = a.m.chunk_words;
+  uint32_t wmap_words = a.m.wmap_words;
+  int32_t G = a.m.G, N = a.m.N, U = a.m.U;
+  uint32_t geo = (uint32_t)a.m.R | ((uint32_t)a.m.C << 9) | ((uint32_t)a.m.logR << 17) | ((uint32_t)a.S << 21);
+  uint32_t sw_m = (uint32_t)a.SW | ((uint32_t)a.M << 16);
+  void* kargs[] = {&x, &blob, &off_wmap, &tile_words, &chunk_words, &wmap_words, &G, &N, &geo, &U, &sw_m, &args};
   return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
 }
 
