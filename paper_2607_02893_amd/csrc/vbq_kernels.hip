@@ -233,6 +233,14 @@ __device__ __forceinline__ UnitInfo load_unit(const DevMatrix& mat, int t, int k
 __device__ __forceinline__ uint32_t lane_id() {
   return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
 }
+// The lane index, recomputed where it is called: values derived from it are
+// then not hoisted out of the work loop, where they would be held (or
+// spilled) across the whole loop.
+__device__ __forceinline__ uint32_t lane_id_here() {
+  uint32_t l;
+  __asm__ __volatile__("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
@@ -357,6 +365,18 @@ __device__ __forceinline__ uint32_t dpp(uint32_t v) {
 constexpr int kDppShr1 = 0x111, kDppShr2 = 0x112, kDppShr4 = 0x114, kDppShr8 = 0x118;
 constexpr int kDppQuadXor1 = 0xB1, kDppQuadXor2 = 0x4E;  // quad_perm [1,0,3,2] and [2,3,0,1]
 
+// v + (v of a neighbour lane), as floats
+__device__ __forceinline__ float add_dpp_f32_quad_xor1(float s) {
+  return s + __builtin_bit_cast(float, dpp<kDppQuadXor1>(__builtin_bit_cast(uint32_t, s)));
+}
+__device__ __forceinline__ float add_dpp_f32_quad_xor2(float s) {
+  return s + __builtin_bit_cast(float, dpp<kDppQuadXor2>(__builtin_bit_cast(uint32_t, s)));
+}
+__device__ __forceinline__ float add_dpp_f32_shr4(float s) {
+  return s + __builtin_bit_cast(float, dpp<kDppShr4>(__builtin_bit_cast(uint32_t, s)));
+}
+
+
 // Sum over the wave (integers): prefix sums inside each row of 16 lanes,
 // then the four row totals.  The result is wave-uniform.
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
@@ -464,19 +484,21 @@ __device__ __forceinline__ void build_index(const WmapRegs& wr, const UnitInfo& 
 }
 
 // ---------------------------------------------------------------------------
-// Batches.  A wave's batch of class CLS holds E entries per lane: 32 bytes of
-// codes per lane for widths up to 4 bits (4 x 1-bit, 2 x 2-bit, 1 x 4-bit)
-// and one 64-byte entry for 8 bits.  Entry e of the window's class run goes
-// to lane e % 64 of group e / 64; batch b covers groups bE .. bE+E-1, so
-// every load instruction reads one contiguous span.
+// Batches.  Every lane holds 32 bytes of codes per batch: E = 4, 2, 1 whole
+// entries for widths 1, 2, 4, and half an entry for width 8 with one
+// activation row (L = 2 lanes per entry: lanes 2j and 2j+1 hold the low and
+// high halves of one entry; several rows take whole 8-bit entries).  Slot
+// i of batch b covers the run's entries (bE + i) * 64/L .. + 64/L - 1, one per
+// lane (or lane pair), so every load instruction reads one contiguous span.
 // ---------------------------------------------------------------------------
-constexpr int kBatchWords = 8;
-
-template <int CLS>
+template <int CLS, int MT>
 struct Batch {
-  static constexpr int NW = 2 << CLS;                                 // uint32 words per entry
-  static constexpr int E = NW >= kBatchWords ? 1 : kBatchWords / NW;  // entries per lane
-  uint32_t w[E * NW];
+  static constexpr int NW = 2 << CLS;                    // uint32 words per entry
+  static constexpr int L = CLS == 3 && MT == 1 ? 2 : 1;  // lanes per entry
+  static constexpr int E = CLS == 3 ? 1 : 4 >> CLS;     // entry slots per lane
+  static constexpr int LW = NW / L;                // words per lane per slot
+  static constexpr int G = 64 / L;                 // entries per slot across the wave
+  uint32_t w[E * LW];
   uint16_t s[E];
 };
 
@@ -486,29 +508,30 @@ struct Batch {
 // Unconditional loads keep the number of outstanding loads the same on every
 // path, so the compiler waits only for the batch it is about to decode and
 // later batches stay in flight (a conditional load makes it wait for all).
-template <int CLS>
-__device__ __forceinline__ void load_batch(Batch<CLS>& bt, const DevMatrix& mat, uint32_t start, int n, int b,
+template <int CLS, int MT>
+__device__ __forceinline__ void load_batch(Batch<CLS, MT>& bt, const DevMatrix& mat, uint32_t start, int n, int b,
                                            uint32_t lane) {
-  constexpr int NW = Batch<CLS>::NW, E = Batch<CLS>::E;
+  using BT = Batch<CLS, MT>;
   const uint32_t lim = max(mat.n_entries[CLS], 1u) - 1u;
+  const uint32_t half = BT::L == 2 ? (lane & 1u) : 0u;
 #pragma unroll
-  for (int i = 0; i < E; ++i) {
-    const int e = max(min((b * E + i) * 64 + (int)lane, n - 1), 0);
+  for (int i = 0; i < BT::E; ++i) {
+    const int e = max(min((b * BT::E + i) * BT::G + (int)(lane / BT::L), n - 1), 0);
     const uint32_t g = min(start + (uint32_t)e, lim);
     bt.s[i] = ld<uint16_t>(mat.blob, mat.off_scales[CLS] + 2u * g);
-    const uint32_t off = mat.off_codes[CLS] + g * (4u * NW);
-    if constexpr (NW == 2) {
+    const uint32_t off = mat.off_codes[CLS] + g * (4u * BT::NW) + half * (4u * BT::LW);
+    if constexpr (BT::LW == 2) {
       const u32x2 v = ld_nt<u32x2>(mat.blob, off);
       bt.w[2 * i] = v.x;
       bt.w[2 * i + 1] = v.y;
     } else {
 #pragma unroll
-      for (int k = 0; k < NW / 4; ++k) {
+      for (int k = 0; k < BT::LW / 4; ++k) {
         const u32x4 v = ld_nt<u32x4>(mat.blob, off + 16u * k);
-        bt.w[i * NW + 4 * k] = v.x;
-        bt.w[i * NW + 4 * k + 1] = v.y;
-        bt.w[i * NW + 4 * k + 2] = v.z;
-        bt.w[i * NW + 4 * k + 3] = v.w;
+        bt.w[i * BT::LW + 4 * k] = v.x;
+        bt.w[i * BT::LW + 4 * k + 1] = v.y;
+        bt.w[i * BT::LW + 4 * k + 2] = v.z;
+        bt.w[i * BT::LW + 4 * k + 3] = v.w;
       }
     }
   }
@@ -534,19 +557,23 @@ __device__ constexpr int first_pair_of_slot(int sl) {
 // product(s) to LDS.  Lanes past the end of a run hold a copy of the run's
 // last entry (clamped loads), so they store the same value to the same place.
 template <int CLS, int MT>
-__device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits, int p, bool valid, const Win& wn) {
+__device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits, int p, bool valid, uint32_t lane,
+                                              const Win& wn) {
   using D = DecFor<CLS, MT>;
+  constexpr int L = Batch<CLS, MT>::L;
+  constexpr int NQ = 8 / L;  // x chunks (4 pairs each) this lane covers
   const int js = p >> wn.logR;
-  const uint32_t xaddr = wn.xs + (uint32_t)__umul24((uint32_t)js, kXStride);
+  // lane pairs of a half-entry class: the odd lane takes the high half
+  const uint32_t xaddr = wn.xs + (uint32_t)__umul24((uint32_t)js, kXStride) + (L == 2 ? (lane & 1u) * 64u : 0u);
   float acc[MT][D::kSlots];
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {  // x chunk q holds pairs 4q..4q+3
+  for (int q = 0; q < NQ; ++q) {  // local x chunk q holds pairs 4q..4q+3 of this lane's share
     u32x4 xv[MT];
 #pragma unroll
     for (int m = 0; m < MT; ++m) xv[m] = lds_u32x4(xaddr + (uint32_t)m * wn.xstride_m + 16u * q);
 #pragma unroll
     for (int c4 = 0; c4 < 4; ++c4) {
-      const int i = 4 * q + c4;
+      const int i = 4 * q + c4;  // pair index within the lane's share (the field table repeats per word)
       const int wi = i / D::kFields, f = i % D::kFields;
       constexpr uint32_t one = (1u << D::B) - 1;
       const Field fd = D::field(f);
@@ -569,6 +596,7 @@ __device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits
     float su = acc[m][0] * D::inv_value(0);
 #pragma unroll
     for (int k = 1; k < D::kSlots; ++k) su = __builtin_fmaf(acc[m][k], D::inv_value(k), su);
+    if constexpr (L == 2) su = add_dpp_f32_quad_xor1(su);  // both halves, the same sum in both lanes
     const float X = lds_f32(wn.Xs + 4u * (uint32_t)(m * wn.SW + js));
     const float sq = CLS == 0 ? __builtin_fmaf(su, 2.0f, -X) : __builtin_fmaf(-(float)(1 << (D::B - 1)), X, su);
     // (several rows: skipping the duplicates keeps the register allocator's
@@ -578,18 +606,18 @@ __device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits
 }
 
 template <int CLS, int MT>
-__device__ __forceinline__ void decode_batch(const Batch<CLS>& bt, uint32_t inv_c, int n, int b, uint32_t lane,
+__device__ __forceinline__ void decode_batch(const Batch<CLS, MT>& bt, uint32_t inv_c, int n, int b, uint32_t lane,
                                              const Win& wn) {
-  constexpr int NW = Batch<CLS>::NW, E = Batch<CLS>::E;
-  int p[E];
+  using BT = Batch<CLS, MT>;
+  int p[BT::E];
 #pragma unroll
-  for (int i = 0; i < E; ++i)
-    p[i] = lds_u16(inv_c + 2u * (uint32_t)max(min((b * E + i) * 64 + (int)lane, n - 1), 0));
+  for (int i = 0; i < BT::E; ++i)
+    p[i] = lds_u16(inv_c + 2u * (uint32_t)max(min((b * BT::E + i) * BT::G + (int)(lane / BT::L), n - 1), 0));
 #pragma unroll
-  for (int i = 0; i < E; ++i) {
-    const int g0 = (b * E + i) * 64;
-    if (g0 < n)  // wave-uniform: whole groups past the end are skipped
-      compute_entry<CLS, MT>(&bt.w[i * NW], bt.s[i], p[i], g0 + (int)lane < n, wn);
+  for (int i = 0; i < BT::E; ++i) {
+    const int g0 = (b * BT::E + i) * BT::G;
+    if (g0 < n)  // wave-uniform: whole slots past the end are skipped
+      compute_entry<CLS, MT>(&bt.w[i * BT::LW], bt.s[i], p[i], g0 + (int)(lane / BT::L) < n, lane, wn);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
@@ -601,16 +629,16 @@ __device__ __forceinline__ void decode_batch(const Batch<CLS>& bt, uint32_t inv_
 // (past the last batch they repeat it), so the count of outstanding loads
 // never depends on the data.
 template <int CLS, int MT>
-__device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS>& A, uint32_t start, int n,
+__device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS, MT>& A, uint32_t start, int n,
                                           uint32_t inv_c, const Win& wn, uint32_t lane) {
-  constexpr int per_batch = Batch<CLS>::E * 64;
+  constexpr int per_batch = Batch<CLS, MT>::E * Batch<CLS, MT>::G;
   const int nb = max(1, (n + per_batch - 1) / per_batch);
-  Batch<CLS> B;
+  Batch<CLS, MT> B;
   for (int b = 0; b < nb; b += 2) {
-    load_batch<CLS>(B, mat, start, n, min(b + 1, nb - 1), lane);
+    load_batch<CLS, MT>(B, mat, start, n, min(b + 1, nb - 1), lane);
     decode_batch<CLS, MT>(A, inv_c, n, b, lane, wn);
     if (b + 1 >= nb) break;
-    load_batch<CLS>(A, mat, start, n, min(b + 2, nb - 1), lane);
+    load_batch<CLS, MT>(A, mat, start, n, min(b + 2, nb - 1), lane);
     decode_batch<CLS, MT>(B, inv_c, n, b + 1, lane, wn);
   }
 }
@@ -634,16 +662,6 @@ __device__ __forceinline__ void load_x1(const uint16_t* __restrict__ x, int j, i
 // lane sums its chunk, the lanes of each quad add their sums pairwise
 // (xor 1, then xor 2), and the last lane of the column's eight adds the
 // first quad's sum to its own (a fixed order).
-__device__ __forceinline__ float add_dpp_f32_quad_xor1(float s) {
-  return s + __builtin_bit_cast(float, dpp<kDppQuadXor1>(__builtin_bit_cast(uint32_t, s)));
-}
-__device__ __forceinline__ float add_dpp_f32_quad_xor2(float s) {
-  return s + __builtin_bit_cast(float, dpp<kDppQuadXor2>(__builtin_bit_cast(uint32_t, s)));
-}
-__device__ __forceinline__ float add_dpp_f32_shr4(float s) {
-  return s + __builtin_bit_cast(float, dpp<kDppShr4>(__builtin_bit_cast(uint32_t, s)));
-}
-
 __device__ __forceinline__ void store_x1(int cols, const XRegs& xr, const Win& wn, uint32_t lane) {
   const int n = cols * 8;
   const uint32_t ones = 0x3C003C00u;  // (1.0, 1.0)
@@ -780,6 +798,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
   for (int i = (int)lane; i < NS; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
 
   for (int item = wave; item < mat.U * S; item += NW) {
+    const uint32_t lane = lane_id_here();
     const int k = item / S, sl = item - k * S;
     const UnitInfo u = load_unit(mat, t, k);
     const int unit = t * mat.U + k;
@@ -807,26 +826,28 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
         seg[c] = inv + 2u * o;
         o += wc.own[c];
       }
-      // the first batches of the 1-, 2- and 4-bit classes are in flight while
-      // the index is built and x is staged (the 8-bit one, twice as wide,
-      // would not fit the register budget and is loaded when its turn comes)
-      Batch<0> A0;
-      Batch<1> A1;
-      Batch<2> A2;
-      Batch<3> A3;
-      load_batch<0>(A0, mat, start[0], n[0], 0, lane);
-      load_batch<1>(A1, mat, start[1], n[1], 0, lane);
-      load_batch<2>(A2, mat, start[2], n[2], 0, lane);
+      // one row: x arrived with the map, so it goes to LDS now, freeing its
+      // registers before the code batches are loaded
+      if constexpr (MT == 1) store_x1(cols, xr, wn, lane);
+      // the first batch of every class is in flight while the index is built
+      // (and, for several rows, x is staged): one memory latency for all four
+      // (several rows need the registers, and load the 8-bit one when its
+      // turn comes)
+      Batch<0, MT> A0;
+      Batch<1, MT> A1;
+      Batch<2, MT> A2;
+      Batch<3, MT> A3;
+      load_batch<0, MT>(A0, mat, start[0], n[0], 0, lane);
+      load_batch<1, MT>(A1, mat, start[1], n[1], 0, lane);
+      load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
+      if constexpr (MT == 1) load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
       build_index(wr, u, wb, we, R, wc, inv, lane);
-      if constexpr (MT == 1)
-        store_x1(cols, xr, wn, lane);
-      else
-        stage_x<MT>(a, u.j0 + c0, cols, wn, lane);
+      if constexpr (MT > 1) stage_x<MT>(a, u.j0 + c0, cols, wn, lane);
       lds_phase();
       run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
       run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
       run_class<2, MT>(mat, A2, start[2], n[2], seg[2], wn, lane);
-      load_batch<3>(A3, mat, start[3], n[3], 0, lane);
+      if constexpr (MT > 1) load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
       run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
       lds_phase();
       reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
