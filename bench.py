@@ -214,6 +214,7 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=3)
+    ap.add_argument("--batch", type=int, default=1, help="activation rows M (M > 1 times vbq_gemm_small)")
     ap.add_argument("--workers", type=int, default=min(12, len(os.sched_getaffinity(0))))
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
@@ -247,8 +248,10 @@ def main():
         desc = vbq.VbqDesc.from_buffer_copy(dbytes)
         Wp = vbq.PackedMatrix(blob, desc, device=dev)
         spec = wl.matrices[idx]
-        x = torch.from_numpy(np.ascontiguousarray(synth.make_x(spec, wl.seed)[0])).to(dev)
-        y = torch.empty(spec.N, dtype=torch.float32, device=dev)
+        xm = synth.make_x(spec, wl.seed, args.batch)
+        x = torch.from_numpy(np.ascontiguousarray(xm[0] if args.batch == 1 else xm)).to(dev)
+        y = torch.empty(spec.N if args.batch == 1 else (args.batch, spec.N), dtype=torch.float32, device=dev)
+        alg += (2 * spec.K + 4 * spec.N) * (args.batch - 1)  # x and y of the extra rows
         mats.append((Wp, x, y, alg))
         total_alg += alg
         total_w += nw
@@ -258,12 +261,18 @@ def main():
     sptr = stream.cuda_stream
 
     launch_args = [(m[0].desc, m[0].blob.data_ptr(), m[1].data_ptr(), m[2].data_ptr()) for m in mats]
+    M = args.batch
+
+    def launch(d, b, x, y, stream_ptr):
+        if M == 1:
+            return vbq.raw_gemv(d, b, x, y, stream_ptr)
+        return vbq.raw_gemm_small(d, b, M, x, d.K, y, d.N, stream_ptr)
 
     def step():
         for d, b, x, y in launch_args:
-            st = vbq.raw_gemv(d, b, x, y, sptr)
+            st = launch(d, b, x, y, sptr)
             if st != 0:
-                raise vbq.VbqError(st, "vbq_gemv")
+                raise vbq.VbqError(st, "vbq_gemv / vbq_gemm_small")
 
     log(f"{len(mats)} GEMVs, {total_w / 1e9:.2f}G weights, algorithmic {total_alg / 1e6:.1f} MB/step, "
         f"blobs {blob_bytes / 1e6:.1f} MB")
@@ -315,7 +324,7 @@ def main():
             csp = cap.cuda_stream
             g.capture_begin()
             for d, b, x, y in launch_args:
-                st = vbq.raw_gemv(d, b, x, y, csp)
+                st = launch(d, b, x, y, csp)
                 if st != 0:
                     raise vbq.VbqError(st, "vbq_gemv (capture)")
             g.capture_end()
@@ -348,7 +357,7 @@ def main():
     for r in range(n_ev):
         for i, (d, b, x, y) in enumerate(launch_args):
             starts[r][i].record(stream)
-            vbq.raw_gemv(d, b, x, y, sptr)
+            launch(d, b, x, y, sptr)
             ends[r][i].record(stream)
     torch.cuda.synchronize()
     dur = np.median(np.array([[starts[r][i].elapsed_time(ends[r][i]) * 1e-3 for i in range(len(mats))]
@@ -372,7 +381,7 @@ def main():
             for Wp, x, y, _ in mats:
                 ws.append(Wp.dequant().half())
             torch.cuda.synchronize()
-            xs = [m[1].view(1, -1) for m in mats]
+            xs = [m[1].view(M, -1) for m in mats]
 
             def dense_step():
                 for w, xx in zip(ws, xs):
@@ -416,7 +425,7 @@ def main():
         "precision": "fp16 activations x {1,2,4,8}-bit codes with fp16 group scales, fp32 accumulation",
         "data": "synthetic (seeded draws; no trained weights)",
         "config": {"workload": f"{wl.name} decode step (workload {args.workload}): {len(mats)} GEMVs, "
-                               f"{total_w / 1e9:.2f}G weights", "M": 1,
+                               f"{total_w / 1e9:.2f}G weights", "M": M,
                    "algorithmic_bytes_per_step": int(total_alg), "blob_bytes": int(blob_bytes),
                    "timing": "HIP-graph replay of the step" if graph_s is not None else "eager launches"},
         "us_per_step": round(1e6 * wall_s, 2),
@@ -425,7 +434,8 @@ def main():
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                     "kernel": "vbq_mv_kernel<1>", "launches_per_step": len(mats),
+                     "kernel": f"vbq_mv_kernel<{1 if M == 1 else 2 if M == 2 else 4 if M <= 4 else 8 if M <= 8 else 16}>",
+                     "launches_per_step": len(mats),
                      "algorithmic_bytes_per_launch": round(alg_per_launch),
                      "avg_launch_us": round(1e6 * per_launch_s, 3),
                      "timing": "HIP events on the launch stream around the timed region / launches",
