@@ -443,7 +443,9 @@ __device__ __forceinline__ WinCounts window_counts(const WmapRegs& wr, const Uni
 // conditions), and real positions write their slot.  No branch depends on
 // the data.  Words whose 64 positions are all real (every word but a unit's
 // last one, outside the ragged last tile) skip the validity masks.
-template <bool kFull>
+// kFwd: write the other direction instead, fwd[pos] = (class << 14) | rank of
+// the position inside its class (run[] then starts at 0 for every class).
+template <bool kFull, bool kFwd = false>
 __device__ __forceinline__ void index_word(uint64_t p0, uint64_t p1, uint64_t valid, uint32_t pos, uint32_t run[4],
                                            uint32_t inv) {
   uint64_t m[4];
@@ -459,32 +461,36 @@ __device__ __forceinline__ void index_word(uint64_t p0, uint64_t p1, uint64_t va
 #pragma unroll
   for (int c = 0; c < 4; ++c)
     slot[c] = __builtin_amdgcn_mbcnt_hi((uint32_t)(m[c] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m[c], run[c]));
-  uint32_t k = slot[3];
-  k = __builtin_amdgcn_inverse_ballot_w64(m[2]) ? slot[2] : k;
-  k = __builtin_amdgcn_inverse_ballot_w64(m[1]) ? slot[1] : k;
+  uint32_t k = slot[3] | (kFwd ? 3u << 14 : 0u);
+  k = __builtin_amdgcn_inverse_ballot_w64(m[2]) ? slot[2] | (kFwd ? 2u << 14 : 0u) : k;
+  k = __builtin_amdgcn_inverse_ballot_w64(m[1]) ? slot[1] | (kFwd ? 1u << 14 : 0u) : k;
   k = __builtin_amdgcn_inverse_ballot_w64(m[0]) ? slot[0] : k;
-  if (kFull || __builtin_amdgcn_inverse_ballot_w64(valid)) lds_store_u16(inv + 2u * k, (uint16_t)pos);
+  if constexpr (kFwd)
+    lds_store_u16(inv + 2u * pos, (uint16_t)(__builtin_amdgcn_inverse_ballot_w64(valid) ? k : 0u));
+  else if (kFull || __builtin_amdgcn_inverse_ballot_w64(valid))
+    lds_store_u16(inv + 2u * k, (uint16_t)pos);
 #pragma unroll
   for (int c = 0; c < 4; ++c) run[c] += (uint32_t)__popcll(m[c]);
 }
 
+template <bool kFwd = false>
 __device__ __forceinline__ void build_index(const WmapRegs& wr, const UnitInfo& u, int wb, int we, int R,
                                             const WinCounts& wc, uint32_t inv, uint32_t lane) {
   uint32_t run[4];
   run[0] = 0;
-  run[1] = wc.own[0];
-  run[2] = run[1] + wc.own[1];
-  run[3] = run[2] + wc.own[2];
+  run[1] = kFwd ? 0u : wc.own[0];
+  run[2] = kFwd ? 0u : run[1] + wc.own[1];
+  run[3] = kFwd ? 0u : run[2] + wc.own[2];
   const int full_end = u.rows == R ? max(wb, min(we, u.npos >> 6)) : wb;
   const uint32_t pos0 = lane - (uint32_t)wb * 64u;
   // words held in lanes w (planes a0/a1) and w - 64 (planes b0/b1)
   for (int w = wb; w < min(full_end, 64); ++w)
-    index_word<true>(read_lane64(wr.a0, w), read_lane64(wr.a1, w), ~0ull, pos0 + 64u * w, run, inv);
+    index_word<true, kFwd>(read_lane64(wr.a0, w), read_lane64(wr.a1, w), ~0ull, pos0 + 64u * w, run, inv);
   for (int w = max(wb, 64); w < full_end; ++w)
-    index_word<true>(read_lane64(wr.b0, w - 64), read_lane64(wr.b1, w - 64), ~0ull, pos0 + 64u * w, run, inv);
+    index_word<true, kFwd>(read_lane64(wr.b0, w - 64), read_lane64(wr.b1, w - 64), ~0ull, pos0 + 64u * w, run, inv);
   for (int w = full_end; w < we; ++w) {
     const bool hi = w >= 64;
-    index_word<false>(read_lane64(hi ? wr.b0 : wr.a0, w & 63), read_lane64(hi ? wr.b1 : wr.a1, w & 63),
+    index_word<false, kFwd>(read_lane64(hi ? wr.b0 : wr.a0, w & 63), read_lane64(hi ? wr.b1 : wr.a1, w & 63),
                       valid_mask(w, u.npos, R, u.rows), pos0 + 64u * w, run, inv);
   }
 }
@@ -881,31 +887,28 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
 // ---------------------------------------------------------------------------
 // Several activation rows (3 <= M <= 16): matrix cores.
 //
-// Y[m][n] = sum_k w_hat[n][k] X[m][k] is computed as 16 x 16 x 16 fp16 MFMA
-// products D[m][e] = sum_k X[m][k] q_e[k] over blocks of up to 16 entries e
-// of one width class that share a group column (hence the same 64
-// activations):
-//   * A (16 x 16, m x k): X rows read straight from global memory (a few
-//     hundred KB at most, L2-resident).  The k order inside each product is
-//     free as long as A and B agree: lane l of product kb holds group
-//     positions 16 (l / 16) + 4 kb .. + 3, so over the four products a lane
-//     covers 16 consecutive activations (two 16-byte loads) and one 16-byte
-//     span of the entry's codes;
-//   * B (16 x 16, k x e): the levels q of entry l % 16 for the same k, made
-//     exactly in fp16: a code field ORed into the mantissa of 1024.0 reads as
-//     1024 + u, and packed fp16 adds give q;
-//   * D: lane l holds D[4 (l / 16) + j][l % 16], j = 0..3.
-// q is exact, so s * D is the entry's product, with no offset term.  Each
-// entry's products for its 16 rows are added to the wave's row sums in block
-// table order (class, then column), a fixed order, so results are bitwise
-// repeatable.
+// Y[m][n] = sum_k w_hat[n][k] X[m][k] as 16 x 16 x 16 fp16 MFMA products
+// D[m][r] = sum_k X[m][k] q_r[k] over the 16 entries r of one group column
+// and 16 consecutive rows (a "block"), whatever their widths:
+//   * lane l works for weight row r = l % 16 and, over the four products kb,
+//     for group positions 16 (l/16) .. + 15 (product kb takes 16 (l/16) + 4 kb
+//     .. + 3: the k order inside a product is free as long as A and B agree);
+//   * A: activations X[l % 16][64 col + 16 (l/16) ..] (two 16-byte loads);
+//   * B: the levels q of row r's entry, made exactly in fp16: a code field ORed
+//     into the mantissa of 1024.0 reads as 1024 + u, and packed fp16 adds give
+//     q.  Each lane decodes its own entry's width with per-lane field
+//     positions, masks and offsets, so every lane runs the same code;
+//   * D: lane l holds D[4 (l/16) + j][l % 16], j = 0..3, so each lane adds
+//     s * D for its weight row and four activation rows to registers over the
+//     slice's columns, in column order (results are bitwise repeatable).
+// A position's entry comes from a per-slice map position -> (class, rank in
+// the slice's class run) built from the width map.
 // ---------------------------------------------------------------------------
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kMmRows = 16;
-constexpr int kMmMaxCols = 32;     // group columns of a slice
-constexpr int kMmMaxBlocks = 256;  // block-table entries of a slice (<= cols * (R/16 + 4))
+constexpr int kMmMaxCols = 32;  // group columns of a slice
 
 struct MmArgs {
   DevMatrix m;
@@ -916,194 +919,100 @@ struct MmArgs {
   int32_t S;          // slices per unit
 };
 
-// Bytes of one wave's LDS region: row sums (16 x R floats), the index
-// (uint16 per position of the slice), the block table.
+// Bytes of one wave's LDS region: row sums (16 x R floats) and the
+// position -> entry map (uint16 per position of the widest slice).
 __host__ __device__ inline int mm_wave_bytes(int R, int cols) {
-  return kMmRows * R * 4 + align16(((cols * R + 63) / 64) * 64 * 2) + kMmMaxBlocks * 4;
+  return kMmRows * R * 4 + align16(((cols * R + 63) / 64) * 64 * 2);
 }
 
-// Inclusive prefix sum over the wave's lanes (integers).
-__device__ __forceinline__ uint32_t wave_prefix(uint32_t v) {
-  v += dpp<kDppShr1>(v);
-  v += dpp<kDppShr2>(v);
-  v += dpp<kDppShr4>(v);
-  v += dpp<kDppShr8>(v);
-  const uint32_t r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31),
-                 r2 = __builtin_amdgcn_readlane(v, 47);
-  const uint32_t row = lane_id_here() >> 4;
-  return v + (row > 0 ? r0 : 0u) + (row > 1 ? r1 : 0u) + (row > 2 ? r2 : 0u);
-}
-
-__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
-  const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src, 64), hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src, 64);
-  return ((uint64_t)hi << 32) | lo;
-}
-
-// Block table of a slice: lane j counts the class-c entries of column j (the
-// column's bits of the width map), prefix sums give each column's first entry
-// in the slice's class run and its first block; each lane then writes its
-// blocks (class-major, columns ascending): entry start (16 bits), count - 1
-// (4), column (6), class (2).  Returns the number of blocks.
-__device__ __forceinline__ int build_mm_blocks(const WmapRegs& wr, const UnitInfo& u, int wb, int cols, int R,
-                                               uint32_t table, uint32_t lane) {
-  uint32_t n01 = 0, n23 = 0;
-  // every lane takes part in the cross-lane reads (a lane permute returns 0
-  // from a lane that is switched off); lanes past the slice count nothing
-  const bool real = (int)lane < cols;
-  const int jl = real ? (int)lane : 0;
-  const int wpc = R > 64 ? R / 64 : 1;  // map words per column
-  for (int i = 0; i < wpc; ++i) {
-    const int w = wb + (R > 64 ? jl * wpc + i : ((jl * R) >> 6));
-    const uint64_t a0 = shfl64(wr.a0, w & 63), b0 = shfl64(wr.b0, w & 63);
-    const uint64_t a1 = shfl64(wr.a1, w & 63), b1 = shfl64(wr.b1, w & 63);
-    const uint64_t p0 = w >= 64 ? b0 : a0, p1 = w >= 64 ? b1 : a1;
-    const int o = R >= 64 ? 0 : ((jl * R) & 63);
-    const uint64_t colmask = !real ? 0ull : R >= 64 ? ~0ull : (((1ull << R) - 1ull) << o);
-    uint64_t m[4];
-    class_masks(p0, p1, valid_mask(w, u.npos, R, u.rows) & colmask, m);
-    n01 += (uint32_t)__popcll(m[0]) | ((uint32_t)__popcll(m[1]) << 16);
-    n23 += (uint32_t)__popcll(m[2]) | ((uint32_t)__popcll(m[3]) << 16);
-  }
-  const uint32_t nb01 = ((n01 & 0xFFFF) + 15) / 16 | ((((n01 >> 16) + 15) / 16) << 16);
-  const uint32_t nb23 = ((n23 & 0xFFFF) + 15) / 16 | ((((n23 >> 16) + 15) / 16) << 16);
-  const uint32_t e01 = wave_prefix(n01) - n01, e23 = wave_prefix(n23) - n23;       // exclusive
-  const uint32_t b01i = wave_prefix(nb01), b23i = wave_prefix(nb23);                // inclusive
-  const uint32_t b01 = b01i - nb01, b23 = b23i - nb23;
-  const uint32_t t01 = __builtin_amdgcn_readlane(b01i, 63), t23 = __builtin_amdgcn_readlane(b23i, 63);
-  const uint32_t tot[4] = {t01 & 0xFFFF, t01 >> 16, t23 & 0xFFFF, t23 >> 16};
-  const uint32_t n[4] = {n01 & 0xFFFF, n01 >> 16, n23 & 0xFFFF, n23 >> 16};
-  const uint32_t e[4] = {e01 & 0xFFFF, e01 >> 16, e23 & 0xFFFF, e23 >> 16};
-  const uint32_t bo[4] = {b01 & 0xFFFF, b01 >> 16, b23 & 0xFFFF, b23 >> 16};
-  uint32_t cls_off = 0;
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    for (uint32_t b = 0; 16 * b < n[c]; ++b) {
-      const uint32_t cnt = min(16u, n[c] - 16 * b);
-      const uint32_t info = (e[c] + 16 * b) | ((cnt - 1) << 16) | (lane << 20) | ((uint32_t)c << 26);
-      lds_store_u32(table + 4u * min(cls_off + bo[c] + b, (uint32_t)kMmMaxBlocks - 1), info);
-    }
-    cls_off += tot[c];
-  }
-  return (int)min(cls_off, (uint32_t)kMmMaxBlocks);
-}
-
-// One block in registers: its table entry, the 16 code bytes that hold this
-// lane's 16 levels, the entry's scale and position, and the lane's 16
-// activations of row l % 16 for the block's column.
-struct MmBlock {
-  uint32_t info;
-  u32x4 w;
-  uint16_t s;
-  int p;
-  u32x4 a0, a1;
-};
-
-// Per-class values of the slice, held in registers for the block loop.
+// Per-class values of the slice.
 struct MmClassInfo {
   uint32_t start[4];  // first entry of the slice's run in each class section
   uint32_t lim[4];    // last entry of each class section (0 when empty)
   uint32_t offc[4], offs[4];
-  uint32_t seg[4];    // first index entry of each class in the slice's index
 };
 
-// v[c] without a branch or a memory access (c is wave-uniform).
-__device__ __forceinline__ uint32_t pick4(const uint32_t v[4], uint32_t c) {
-  const uint32_t m0 = 0u - (uint32_t)(c == 0), m1 = 0u - (uint32_t)(c == 1), m2 = 0u - (uint32_t)(c == 2),
-                 m3 = 0u - (uint32_t)(c == 3);
-  return (v[0] & m0) | (v[1] & m1) | (v[2] & m2) | (v[3] & m3);
+// v[c] for a per-lane c, without memory access.
+__device__ __forceinline__ uint32_t sel4(const uint32_t v[4], uint32_t c) {
+  const uint32_t lo = (c & 1u) ? v[1] : v[0], hi = (c & 1u) ? v[3] : v[2];
+  return (c & 2u) ? hi : lo;
 }
 
-// Loads one block: this lane's entry is e = lane % 16 of the block and it
-// takes the entry's levels 16h .. 16h + 15 (h = lane / 16), i.e. pairs 8h ..
-// 8h + 7, whose codes start at byte (2h << c) & ~3 of the entry (c = width
-// class).  Every load is unconditional and no address depends on a branch,
-// so the compiler can keep several blocks in flight.
-__device__ __forceinline__ void load_mm_block(MmBlock& bk, const MmArgs& a, const DevMatrix& mat, uint32_t table,
-                                              uint32_t inv, int blk, const MmClassInfo& ci, int j0, uint32_t lane) {
-  bk.info = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_u32(table + 4u * (uint32_t)blk));
-  const uint32_t e_start = bk.info & 0xFFFF, cnt = ((bk.info >> 16) & 0xF) + 1, col = (bk.info >> 20) & 0x3F;
-  const uint32_t c = bk.info >> 26;
+// One block in registers for this lane: its entry's 16 code bytes that hold
+// the lane's 16 levels, the width class, the scale (0 for a padding row), and
+// 16 activations of row l % 16.
+struct MmBlock {
+  u32x4 w;
+  uint32_t c;
+  uint16_t s;
+  u32x4 a0, a1;
+};
+
+// Block f of the row group: column f / RB, row block rg*RB + f % RB.  The
+// lane's levels 16h .. 16h + 15 (h = lane / 16) are pairs 8h .. 8h + 7, whose
+// codes start at byte (2h << c) & ~3 of the entry.  Loads are unconditional
+// (clamped), so several blocks stay in flight.
+template <int RB>
+__device__ __forceinline__ void load_mm_block(MmBlock& bk, const MmArgs& a, const DevMatrix& mat, uint32_t fwd,
+                                              int f, int rg, int rows, const MmClassInfo& ci, int j0,
+                                              uint32_t lane) {
+  const int R = mat.R;
   const uint32_t e = lane & 15u, h = lane >> 4;
-  const uint32_t k = e_start + min(e, cnt - 1);
-  const uint32_t g = min(pick4(ci.start, c) + k, pick4(ci.lim, c));
-  bk.w = ld<u32x4>(mat.blob, pick4(ci.offc, c) + (g << (3 + c)) + (((2u * h) << c) & ~3u));
-  bk.s = ld<uint16_t>(mat.blob, pick4(ci.offs, c) + 2u * g);
-  bk.p = lds_u16(inv + 2u * (pick4(ci.seg, c) + k));
+  const int col = f / RB;
+  const int row = (rg * RB + f % RB) * 16 + (int)e;
+  const uint32_t v = (uint32_t)lds_u16(fwd + 2u * (uint32_t)(col * R + row));
+  const bool real = row < rows;
+  const uint32_t c = real ? v >> 14 : 0u;
+  const uint32_t g = min(sel4(ci.start, c) + (real ? (v & 0x3FFFu) : 0u), sel4(ci.lim, c));
+  bk.c = c;
+  bk.w = ld<u32x4>(mat.blob, sel4(ci.offc, c) + (g << (3 + c)) + (((2u * h) << c) & ~3u));
+  const uint16_t sb = ld<uint16_t>(mat.blob, sel4(ci.offs, c) + 2u * g);
+  bk.s = real ? sb : (uint16_t)0;
   const int m = min((int)e, a.M - 1);
-  const u32x4* xr = (const u32x4*)(a.x + (size_t)m * a.ldx + (size_t)(j0 + (int)col) * 64 + 16 * h);
+  const u32x4* xr = (const u32x4*)(a.x + (size_t)m * a.ldx + (size_t)(j0 + col) * 64 + 16 * h);
   bk.a0 = xr[0];
   bk.a1 = xr[1];
 }
 
-// Products of one block for width class CLS.  Lane (e, h) supplies, for
-// product kb, levels 16h + 4kb .. + 3 = pairs 8h + 2kb and 8h + 2kb + 1; in
-// the 16 loaded code bytes these are fields f, f + 1 of word wi:
+// s * D of one block.  For product kb the lane's two pairs 8h + 2kb, + 1 are
+// fields f, f + 1 of word wi of its 16 code bytes:
 //   1 bit: wi = 0, f = 8 (h & 1) + 2kb;  2 bits: wi = 0, f = 2kb;
 //   4 bits: wi = kb / 2, f = 2 (kb & 1); 8 bits: wi = kb, f = 0.
-template <int CLS>
 __device__ __forceinline__ float4_t mm_products(const MmBlock& bk, uint32_t h) {
-  constexpr int B = 1 << CLS;
-  constexpr uint32_t mask = ((1u << B) - 1u) * 0x00010001u;
+  const uint32_t c = bk.c, B = 1u << c;
+  const uint32_t mask = (0x00010001u << B) - 0x00010001u;
+  // q = (1024 + u - 1024) * mul + add: mul 2, add -1 for 1 bit; mul 1, add -2^(B-1)
+  const half2_t base = {(_Float16)-1024.0f, (_Float16)-1024.0f};
+  const _Float16 mul1 = c == 0 ? (_Float16)2.0f : (_Float16)1.0f;
+  const _Float16 add1 = c == 0 ? (_Float16)-1.0f : (_Float16)(-(float)(1u << (B - 1)));
+  const half2_t mul = {mul1, mul1}, add = {add1, add1};
   const uint32_t w[4] = {bk.w.x, bk.w.y, bk.w.z, bk.w.w};
   const uint32_t a[8] = {bk.a0.x, bk.a0.y, bk.a0.z, bk.a0.w, bk.a1.x, bk.a1.y, bk.a1.z, bk.a1.w};
   float4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
-    const uint32_t word = CLS <= 1 ? w[0] : CLS == 2 ? w[kb >> 1] : w[kb];
-    const uint32_t f = CLS == 0 ? 8u * (h & 1u) + 2u * kb : CLS == 1 ? 2u * kb : CLS == 2 ? 2u * (kb & 1) : 0u;
-    const uint32_t v0 = ((word >> (f * B)) & mask) | 0x64006400u;  // 1024 + u, both halves
-    const uint32_t v1 = ((word >> ((f + 1) * B)) & mask) | 0x64006400u;
-    half2_t q0 = as_h2(v0), q1 = as_h2(v1);
-    if constexpr (CLS == 0) {  // q = 2u - 1, as (v - 1024) * 2 - 1 (2049 has no fp16 value)
-      const half2_t base = {(_Float16)-1024.0f, (_Float16)-1024.0f}, two = {(_Float16)2.0f, (_Float16)2.0f},
-                    one = {(_Float16)-1.0f, (_Float16)-1.0f};
-      q0 = (q0 + base) * two + one;
-      q1 = (q1 + base) * two + one;
-    } else {  // q = u - 2^(B-1)
-      const _Float16 o = (_Float16)(-(1024.0f + (float)(1 << (B - 1))));
-      const half2_t off = {o, o};
-      q0 = q0 + off;
-      q1 = q1 + off;
-    }
+    const uint32_t word = c == 3 ? w[kb] : c == 2 ? w[kb >> 1] : w[0];
+    const uint32_t f = c == 0 ? 8u * (h & 1u) + 2u * kb : c == 1 ? 2u * kb : c == 2 ? 2u * (kb & 1) : 0u;
+    const uint32_t sh = f << c;
+    const uint32_t v0 = ((word >> sh) & mask) | 0x64006400u;  // 1024 + u, both halves
+    const uint32_t v1 = ((word >> (sh + B)) & mask) | 0x64006400u;
+    const half2_t q0 = (as_h2(v0) + base) * mul + add, q1 = (as_h2(v1) + base) * mul + add;
     const half4_t bq = {q0.x, q0.y, q1.x, q1.y};
     const half4_t ax = __builtin_bit_cast(half4_t, u32x2{a[2 * kb], a[2 * kb + 1]});
     d = __builtin_amdgcn_mfma_f32_16x16x16f16(ax, bq, d, 0, 0, 0);
   }
-  return d;
-}
-
-// Adds s * D to the row sums of the block's entries (lanes of real entries
-// and real rows only).
-__device__ __forceinline__ void mm_block(const MmBlock& bk, int R, int M, uint32_t ysum, uint32_t lane) {
-  const uint32_t h = lane >> 4;
-  float4_t d;
-  switch (bk.info >> 26) {
-    case 0: d = mm_products<0>(bk, h); break;
-    case 1: d = mm_products<1>(bk, h); break;
-    case 2: d = mm_products<2>(bk, h); break;
-    default: d = mm_products<3>(bk, h); break;
-  }
-  const uint32_t cnt = ((bk.info >> 16) & 0xF) + 1;
-  const int row = bk.p & (R - 1);
   const float s = (float)__builtin_bit_cast(_Float16, bk.s);
-  if ((lane & 15u) < cnt) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = 4 * (int)h + j;
-      if (m < M) {
-        const uint32_t ya = ysum + 4u * (uint32_t)(m * R + row);
-        lds_store_f32(ya, lds_f32(ya) + s * d[j]);
-      }
-    }
-  }
+  return d * s;
 }
 
-// Marks a block's registers as read here.
+// Marks a block's registers as read here: every buffer's load is consumed on
+// every path, so no register with a load in flight is ever reused for
+// something else (which would make the compiler wait for all loads).
 __device__ __forceinline__ void mm_done(const MmBlock& bk) {
-  __asm__ __volatile__("" ::"v"(bk.w), "v"(bk.s), "v"(bk.a0), "v"(bk.a1));
+  __asm__ __volatile__("" ::"v"(bk.w), "v"(bk.s), "v"(bk.a0), "v"(bk.a1), "v"(bk.c));
 }
 
-template <int NW>
+template <int NW, int RB>
 __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(MmArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const DevMatrix& mat = a.m;
@@ -1112,16 +1021,17 @@ __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(MmArgs a) {
   const int wave = wave_id();
   const int t = blockIdx.x;  // one row tile per workgroup
   const int cmax = max_slice_cols(R, mat.C, S);
-  const uint32_t region = lds0 + (uint32_t)(wave * mm_wave_bytes(R, cmax));
-  const uint32_t ysum = region;
-  const uint32_t inv = region + (uint32_t)(kMmRows * R * 4);
-  const uint32_t table = inv + (uint32_t)align16(((cmax * R + 63) / 64) * 64 * 2);
+  const int wbytes = mm_wave_bytes(R, cmax);
+  const uint32_t ysum = lds0 + (uint32_t)(wave * wbytes);
+  const uint32_t fwd = ysum + (uint32_t)(kMmRows * R * 4);
+  const int rows = min(R, mat.N - t * R);
   {
     const uint32_t lane = lane_id_here();
     for (int i = (int)lane; i < kMmRows * R; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
   }
   for (int item = wave; item < mat.U * S; item += NW) {
     const uint32_t lane = lane_id_here();
+    const uint32_t h = lane >> 4;
     const int k = item / S, sl = item - k * S;
     const UnitInfo u = load_unit(mat, t, k);
     const int unit = t * mat.U + k;
@@ -1132,53 +1042,61 @@ __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(MmArgs a) {
     const WmapRegs wr = load_wmap(mat, u, we, lane);
     const WinCounts wc = window_counts(wr, u, wb, we, R, lane);
     MmClassInfo ci;
-    uint32_t o = 0;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       ci.start[c] = uniform((int)(class_start(mat, unit, c) + wc.before[c]));
       ci.lim[c] = uniform((int)(max(mat.n_entries[c], 1u) - 1u));
       ci.offc[c] = uniform((int)mat.off_codes[c]);
       ci.offs[c] = uniform((int)mat.off_scales[c]);
-      ci.seg[c] = o;
-      o += wc.own[c];
     }
-    build_index(wr, u, wb, we, R, wc, inv, lane);
-    const int nblk = build_mm_blocks(wr, u, wb, ce - cb, R, table, lane);
+    build_index<true>(wr, u, wb, we, R, wc, fwd, lane);
     lds_phase();
     const int j0 = u.j0 + cb;
-    // four blocks in flight: a block's loads are issued three blocks before
-    // it is used (loads past the last block repeat it, so the number of
-    // outstanding loads never depends on the data)
-    const int last = nblk - 1;
-    MmBlock B0, B1, B2, B3;
-    load_mm_block(B0, a, mat, table, inv, 0, ci, j0, lane);
-    load_mm_block(B1, a, mat, table, inv, min(1, last), ci, j0, lane);
-    load_mm_block(B2, a, mat, table, inv, min(2, last), ci, j0, lane);
-    // Every buffer's load is consumed on every path (mm_done), so no register
-    // with a load in flight is ever reused for something else, which would
-    // make the compiler wait for all outstanding loads.
-    for (int blk = 0; blk < nblk; blk += 4) {
-      load_mm_block(B3, a, mat, table, inv, min(blk + 3, last), ci, j0, lane);
-      mm_block(B0, R, a.M, ysum, lane);
+    const int nf = (ce - cb) * RB;  // blocks per row group
+    const int last = nf - 1;
+    for (int rg = 0; rg < R / (16 * RB); ++rg) {
+      float4_t acc[RB];
+#pragma unroll
+      for (int i = 0; i < RB; ++i) acc[i] = float4_t{0.0f, 0.0f, 0.0f, 0.0f};
+      MmBlock B0, B1, B2, B3;
+      load_mm_block<RB>(B0, a, mat, fwd, 0, rg, rows, ci, j0, lane);
+      load_mm_block<RB>(B1, a, mat, fwd, min(1, last), rg, rows, ci, j0, lane);
+      load_mm_block<RB>(B2, a, mat, fwd, min(2, last), rg, rows, ci, j0, lane);
+      // four blocks in flight; block f adds into acc[f % RB] (the ring slot)
+      for (int f = 0; f < nf; f += 4) {
+        load_mm_block<RB>(B3, a, mat, fwd, min(f + 3, last), rg, rows, ci, j0, lane);
+        acc[0 % RB] += mm_products(B0, h);
+        mm_done(B0);
+        load_mm_block<RB>(B0, a, mat, fwd, min(f + 4, last), rg, rows, ci, j0, lane);
+        if (f + 1 < nf) acc[1 % RB] += mm_products(B1, h);
+        mm_done(B1);
+        load_mm_block<RB>(B1, a, mat, fwd, min(f + 5, last), rg, rows, ci, j0, lane);
+        if (f + 2 < nf) acc[2 % RB] += mm_products(B2, h);
+        mm_done(B2);
+        load_mm_block<RB>(B2, a, mat, fwd, min(f + 6, last), rg, rows, ci, j0, lane);
+        if (f + 3 < nf) acc[3 % RB] += mm_products(B3, h);
+        mm_done(B3);
+      }
       mm_done(B0);
-      load_mm_block(B0, a, mat, table, inv, min(blk + 4, last), ci, j0, lane);
-      if (blk + 1 < nblk) mm_block(B1, R, a.M, ysum, lane);
       mm_done(B1);
-      load_mm_block(B1, a, mat, table, inv, min(blk + 5, last), ci, j0, lane);
-      if (blk + 2 < nblk) mm_block(B2, R, a.M, ysum, lane);
       mm_done(B2);
-      load_mm_block(B2, a, mat, table, inv, min(blk + 6, last), ci, j0, lane);
-      if (blk + 3 < nblk) mm_block(B3, R, a.M, ysum, lane);
-      mm_done(B3);
+      // this wave's share of the row sums (several items add up in order)
+#pragma unroll
+      for (int i = 0; i < RB; ++i) {
+        const int row = (rg * RB + i) * 16 + (int)(lane & 15u);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int m = 4 * (int)h + j;
+          if (m < a.M && row < rows) {
+            const uint32_t ya = ysum + 4u * (uint32_t)(m * R + row);
+            lds_store_f32(ya, lds_f32(ya) + acc[i][j]);
+          }
+        }
+      }
     }
-    mm_done(B0);
-    mm_done(B1);
-    mm_done(B2);
     lds_phase();
   }
   __syncthreads();
-  const int rows = min(R, mat.N - t * R);
-  const int wbytes = mm_wave_bytes(R, cmax);
   for (int slot = threadIdx.x; slot < kMmRows * R; slot += NW * 64) {
     const int m = slot / R, r = slot - m * R;
     if (m < a.M && r < rows) {
@@ -1391,9 +1309,9 @@ vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
 
 // Several rows on matrix cores: same item split as the one-row path (slices
 // of at most 32 columns, at least four items per tile).
-template <int NW>
+template <int NW, int RB>
 vbq_status launch_mm_nw(const MmArgs& a, int lds, hipStream_t s) {
-  const void* kernel = (const void*)vbq_mm_kernel<NW>;
+  const void* kernel = (const void*)vbq_mm_kernel<NW, RB>;
   if (lds > 64 * 1024) {
     static std::atomic<uint64_t> done{0};
     vbq_status st = allow_big_lds(kernel, done);
@@ -1404,11 +1322,17 @@ vbq_status launch_mm_nw(const MmArgs& a, int lds, hipStream_t s) {
   return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
 }
 
+template <int RB>
+vbq_status launch_mm_rb(const MmArgs& a, int NW, int lds, hipStream_t s) {
+  if (NW == 4) return launch_mm_nw<4, RB>(a, lds, s);
+  if (NW == 8) return launch_mm_nw<8, RB>(a, lds, s);
+  return launch_mm_nw<16, RB>(a, lds, s);
+}
+
 vbq_status launch_mm(const DevMatrix& m, const void* x, int64_t ldx, int M, float* y, int64_t ldy, hipStream_t s) {
-  // Each wave walks its blocks one after the other (a chain of dependent
-  // matrix-core and LDS steps), so small matrices split their tiles over
-  // more waves, as long as the whole grid fits the GPU at once (about 20
-  // waves per CU at this kernel's register use).
+  // Each wave walks its blocks one after the other, so small matrices split
+  // their tiles over more waves, as long as the whole grid fits the GPU at
+  // once (about 20 waves per CU at this kernel's register use).
   int NWt = kMinWaves;
   while (NWt < 16 && (int64_t)m.T * NWt * 2 <= 256 * 20) NWt *= 2;
   int S = (NWt + m.U - 1) / m.U;
@@ -1425,9 +1349,10 @@ vbq_status launch_mm(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
   a.ldy = ldy;
   a.M = M;
   a.S = S;
-  if (NW == 4) return launch_mm_nw<4>(a, lds, s);
-  if (NW == 8) return launch_mm_nw<8>(a, lds, s);
-  return launch_mm_nw<16>(a, lds, s);
+  // row blocks of 16 per group: one, two or four (R = 16, 32, >= 64)
+  if (m.R == 16) return launch_mm_rb<1>(a, NW, lds, s);
+  if (m.R == 32) return launch_mm_rb<2>(a, NW, lds, s);
+  return launch_mm_rb<4>(a, NW, lds, s);
 }
 
 }  // namespace
