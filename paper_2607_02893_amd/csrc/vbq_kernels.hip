@@ -154,32 +154,10 @@ struct Dec<3> {
   __device__ static constexpr float inv_value(int) { return 16777216.0f; }  // 2^24
 };
 
-// Single-accumulator tables, used when several activation rows share one
-// decode (M >= 4): every field is moved to one target bit, at one extra shift
-// per field, so each row needs one accumulator instead of one per slot.
-template <int CLS>
-struct Dec1;
-template <>
-struct Dec1<0> {  // every bit to the exponent bit 14: (0, 2.0)
-  static constexpr int B = 1, kFields = 16, kSlots = 1;
-  __device__ static constexpr Field field(int f) { return Field{14 - f, 14}; }
-  __device__ static constexpr int slot(int) { return 0; }
-  __device__ static constexpr float inv_value(int) { return 0.5f; }
-};
-template <>
-struct Dec1<1> {  // every field to bits 8-9: u * 2^-16
-  static constexpr int B = 2, kFields = 8, kSlots = 1;
-  __device__ static constexpr Field field(int f) { return Field{8 - 2 * f, 8}; }
-  __device__ static constexpr int slot(int) { return 0; }
-  __device__ static constexpr float inv_value(int) { return 65536.0f; }
-};
-template <>
-struct Dec1<2> : Dec<2> {};
-template <>
-struct Dec1<3> : Dec<3> {};
-
+// (The one- and two-row dot2 paths both use these tables; three or more rows
+// go to the matrix-core kernel.)
 template <int CLS, int MT>
-using DecFor = typename std::conditional<(MT >= 4), Dec1<CLS>, Dec<CLS>>::type;
+using DecFor = Dec<CLS>;
 
 // ---------------------------------------------------------------------------
 // Index build: positions of each class's entries inside one unit.
@@ -322,12 +300,6 @@ __device__ __forceinline__ void lds_store_u32x4(uint32_t addr, u32x4 v) {
 }
 __device__ __forceinline__ void lds_store_u16(uint32_t addr, uint16_t v) {
   *(__attribute__((address_space(3))) uint16_t*)(size_t)addr = v;
-}
-__device__ __forceinline__ uint32_t lds_u32(uint32_t addr) {
-  return *(const __attribute__((address_space(3))) uint32_t*)(size_t)addr;
-}
-__device__ __forceinline__ void lds_store_u32(uint32_t addr, uint32_t v) {
-  *(__attribute__((address_space(3))) uint32_t*)(size_t)addr = v;
 }
 __device__ __forceinline__ int lds_u16(uint32_t addr) {
   return *(const __attribute__((address_space(3))) uint16_t*)(size_t)addr;
