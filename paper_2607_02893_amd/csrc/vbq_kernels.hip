@@ -1309,9 +1309,10 @@ vbq_status launch_mm(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
   while (NWt < 16 && (int64_t)m.T * NWt * 2 <= 256 * 20) NWt *= 2;
   int S = (NWt + m.U - 1) / m.U;
   while (max_slice_cols(m.R, m.C, S) > kMmMaxCols) ++S;
-  int NW = kMinWaves;
-  while (NW < 16 && NW < m.U * S) NW *= 2;
-  const int lds = NW * mm_wave_bytes(m.R, max_slice_cols(m.R, m.C, S));
+  const int wbytes = mm_wave_bytes(m.R, max_slice_cols(m.R, m.C, S));
+  int NW = kMinWaves;  // (fewer waves than items is fine: items are dealt in turn)
+  while (NW < 16 && NW < m.U * S && 2 * NW * wbytes <= kLdsLimit) NW *= 2;
+  const int lds = NW * wbytes;
   if (lds > kLdsLimit) return VBQ_ERR_UNSUPPORTED;
   MmArgs a;
   a.m = m;

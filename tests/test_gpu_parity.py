@@ -127,6 +127,58 @@ def test_gemm_small_matches_oracle(vbq, M, N, K, R, C):
         parity.check(Y[m], Ystar[m], omatmul.row_magnitude(q, s, X[m]), what=f"gemm m={m}")
 
 
+@pytest.mark.parametrize("M", [3, 16])
+@pytest.mark.parametrize("N,K,R,C", GEOMS)
+def test_gemm_small_all_geometries(vbq, M, N, K, R, C):
+    """Matrix-core path (M >= 3) on every tile height (row groups of 16/32/64
+    rows, several groups per tile for R = 128/256), ragged tiles and chunks."""
+    _say(f"gemm_small geometry M={M} N={N} K={K} R={R} C={C}")
+    spec = synth.MatrixSpec("t", N % 7, K % 5, N, K)
+    bits, q, s = synth.make_matrix(spec, 83)
+    X = synth.make_x(spec, 83, M=M)
+    Y = _packed(vbq, q, s, bits, R, C).gemm_small(_x_dev(X)).cpu().numpy()
+    Ystar = omatmul.gemm(q, s, X)
+    for m in range(M):
+        parity.check(Y[m], Ystar[m], omatmul.row_magnitude(q, s, X[m]), what=f"gemm m={m}")
+
+
+@pytest.mark.parametrize("M", [2, 4, 16])
+def test_gemm_small_one_hot_rows_are_exact(vbq, M):
+    """Row m of X = e_{k_m}: row m of Y is column k_m of w_hat, bit for bit
+    (levels are exact in fp16 and s * q is exact in fp32)."""
+    spec = synth.MatrixSpec("t", 3, 1, 300, 1024)
+    bits, q, s = synth.make_matrix(spec, 89)
+    W = omatmul.dequant(q, s)
+    ks = [(37 * m + 5) % 1024 for m in range(M)]
+    X = np.zeros((M, 1024), dtype=np.float16)
+    for m, k in enumerate(ks):
+        X[m, k] = 1.0
+    Y = _packed(vbq, q, s, bits, 64, 16).gemm_small(_x_dev(X)).cpu().numpy().astype(np.float64)
+    for m, k in enumerate(ks):
+        assert np.array_equal(Y[m], W[:, k]), (m, k)
+
+
+@pytest.mark.parametrize("bits_u", [1, 2, 4, 8])
+def test_gemm_small_uniform_widths(vbq, bits_u):
+    spec = synth.MatrixSpec("t", 1, 4, 160, 2048, uniform_bits=bits_u)
+    bits, q, s = synth.make_matrix(spec, 97)
+    X = synth.make_x(spec, 97, M=8)
+    Y = _packed(vbq, q, s, bits).gemm_small(_x_dev(X)).cpu().numpy()
+    Ystar = omatmul.gemm(q, s, X)
+    for m in range(8):
+        parity.check(Y[m], Ystar[m], omatmul.row_magnitude(q, s, X[m]), what=f"uniform {bits_u} m={m}")
+
+
+def test_gemm_small_bitwise_repeatable(vbq):
+    spec = synth.MatrixSpec("t", 2, 5, 1000, 4096)
+    bits, q, s = synth.make_matrix(spec, 101)
+    Wp = _packed(vbq, q, s, bits)
+    X = _x_dev(synth.make_x(spec, 101, M=16))
+    y0 = Wp.gemm_small(X).cpu().numpy()
+    for _ in range(3):
+        assert np.array_equal(Wp.gemm_small(X).cpu().numpy(), y0)
+
+
 def test_gemm_small_strided_and_empty(vbq):
     spec = synth.MatrixSpec("t", 1, 3, 200, 512)
     bits, q, s = synth.make_matrix(spec, 67)
