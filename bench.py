@@ -116,9 +116,9 @@ def _gen_pack(task):
     return idx, np.asarray(blob).copy(), bytes(desc), alg, spec.N * spec.K
 
 
-def prepare(cfg, workers):
+def prepare(cfg, workers, uniform_bits=0):
     from paper_2607_02893_amd import synth
-    wl = synth.workload(cfg)
+    wl = synth.workload(cfg, uniform_bits) if uniform_bits else synth.workload(cfg)
     tasks = [(i, cfg, wl.seed, m) for i, m in enumerate(wl.matrices)]
     out = [None] * len(tasks)
     t0 = time.time()
@@ -215,6 +215,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--batch", type=int, default=1, help="activation rows M (M > 1 times vbq_gemm_small)")
+    ap.add_argument("--uniform", type=int, default=0, choices=(0, 1, 2, 4, 8),
+                    help="every group of every matrix at this width (the 1.46B workload's roofline variants)")
     ap.add_argument("--workers", type=int, default=min(12, len(os.sched_getaffinity(0))))
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
@@ -234,7 +236,7 @@ def main():
               "(the row / K split that would shard it is described in the design notes).", file=sys.stderr)
         sys.exit(2)
 
-    wl, packed = prepare(args.workload, args.workers)
+    wl, packed = prepare(args.workload, args.workers, args.uniform)
 
     import torch
     from paper_2607_02893_amd import synth, vbq
@@ -426,6 +428,7 @@ def main():
         "data": "synthetic (seeded draws; no trained weights)",
         "config": {"workload": f"{wl.name} decode step (workload {args.workload}): {len(mats)} GEMVs, "
                                f"{total_w / 1e9:.2f}G weights", "M": M,
+                   "uniform_bits": args.uniform or None,
                    "algorithmic_bytes_per_step": int(total_alg), "blob_bytes": int(blob_bytes),
                    "timing": "HIP-graph replay of the step" if graph_s is not None else "eager launches"},
         "us_per_step": round(1e6 * wall_s, 2),

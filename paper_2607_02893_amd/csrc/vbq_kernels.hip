@@ -589,14 +589,23 @@ __device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits
   }
 }
 
-template <int CLS, int MT>
+// kUni: every entry of the window has width CLS, so the k-th one sits at the
+// k-th real position: column k / rows, row k % rows (inv_c is then `rows`).
+template <int CLS, int MT, bool kUni = false>
 __device__ __forceinline__ void decode_batch(const Batch<CLS, MT>& bt, uint32_t inv_c, int n, int b, uint32_t lane,
                                              const Win& wn) {
   using BT = Batch<CLS, MT>;
   int p[BT::E];
 #pragma unroll
-  for (int i = 0; i < BT::E; ++i)
-    p[i] = lds_u16(inv_c + 2u * (uint32_t)max(min((b * BT::E + i) * BT::G + (int)(lane / BT::L), n - 1), 0));
+  for (int i = 0; i < BT::E; ++i) {
+    const int k = max(min((b * BT::E + i) * BT::G + (int)(lane / BT::L), n - 1), 0);
+    if constexpr (kUni) {
+      const int rows = (int)inv_c;
+      p[i] = rows == (1 << wn.logR) ? k : (k / rows) * (1 << wn.logR) + k % rows;
+    } else {
+      p[i] = lds_u16(inv_c + 2u * (uint32_t)k);
+    }
+  }
 #pragma unroll
   for (int i = 0; i < BT::E; ++i) {
     const int g0 = (b * BT::E + i) * BT::G;
@@ -612,7 +621,7 @@ __device__ __forceinline__ void decode_batch(const Batch<CLS, MT>& bt, uint32_t 
 // decoded.  The loop runs at least once and its loads are unconditional
 // (past the last batch they repeat it), so the count of outstanding loads
 // never depends on the data.
-template <int CLS, int MT>
+template <int CLS, int MT, bool kUni = false>
 __device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS, MT>& A, uint32_t start, int n,
                                           uint32_t inv_c, const Win& wn, uint32_t lane) {
   constexpr int per_batch = Batch<CLS, MT>::E * Batch<CLS, MT>::G;
@@ -620,10 +629,10 @@ __device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS, MT>& 
   Batch<CLS, MT> B;
   for (int b = 0; b < nb; b += 2) {
     load_batch<CLS, MT>(B, mat, start, n, min(b + 1, nb - 1), lane);
-    decode_batch<CLS, MT>(A, inv_c, n, b, lane, wn);
+    decode_batch<CLS, MT, kUni>(A, inv_c, n, b, lane, wn);
     if (b + 1 >= nb) break;
     load_batch<CLS, MT>(A, mat, start, n, min(b + 2, nb - 1), lane);
-    decode_batch<CLS, MT>(B, inv_c, n, b + 1, lane, wn);
+    decode_batch<CLS, MT, kUni>(B, inv_c, n, b + 1, lane, wn);
   }
 }
 
@@ -741,7 +750,12 @@ __device__ __forceinline__ int clamp_run(const DevMatrix& mat, int c, uint32_t s
 // kernel-argument fetch.  geo packs R (9 bits), C (8), log2 R (4) and S (8);
 // sw_m packs SW (16) and M (16).  (At most 16 SGPRs can be preloaded, two
 // of which hold the kernel-argument pointer: these eleven take 13.)
-template <int MT, int NW>
+//
+// UNI >= 0: every group of the matrix has width class UNI (a uniform "recipe"
+// matrix, one row only).  Entries then sit at consecutive real positions, so
+// the width map, the class counts and the index are not needed, and a unit's
+// first entry follows from the geometry.
+template <int MT, int NW, int UNI = -1>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 4 : 2))) void vbq_mv_kernel(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ blob, uint32_t off_wmap, uint32_t tile_words,
     uint32_t chunk_words, uint32_t wmap_words, int32_t G, int32_t N, uint32_t geo, int32_t U, uint32_t sw_m,
@@ -790,11 +804,27 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
     slice_cols(u.cols, R, sl, S, cb, ce);
     if (cb >= ce) continue;  // wave-uniform: an empty slice
     const int slice_we = (ce * R + 63) >> 6;
+    XRegs xr;
+    if constexpr (MT == 1) load_x1(a.x, u.j0 + cb, ce - cb, xr, lane);  // with the map: one latency
+    if constexpr (UNI >= 0) {
+      // all tiles above this one are full: R*G entries each; this tile's
+      // units hold C*rows entries each
+      const uint32_t first = (uint32_t)t * (uint32_t)(R * mat.G) + (uint32_t)(u.j0 + cb) * (uint32_t)u.rows;
+      const int cols = ce - cb;
+      const int n = clamp_run(mat, UNI, first, (uint32_t)(cols * u.rows));
+      Batch<UNI, MT> A;
+      load_batch<UNI, MT>(A, mat, first, n, 0, lane);
+      store_x1(cols, xr, wn, lane);
+      lds_phase();
+      run_class<UNI, MT, true>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
+      lds_phase();
+      reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
+      lds_phase();
+      continue;
+    }
     uint32_t ustart[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) ustart[c] = class_start(mat, unit, c);
-    XRegs xr;
-    if constexpr (MT == 1) load_x1(a.x, u.j0 + cb, ce - cb, xr, lane);  // with the map: one latency
     const WmapRegs wr = load_wmap(mat, u, slice_we, lane);
     auto window = [&](int c0, int c1) __attribute__((always_inline)) {
       const int cols = c1 - c0;
@@ -1239,9 +1269,9 @@ vbq_status allow_big_lds(const void* kernel, std::atomic<uint64_t>& done) {
   return st;
 }
 
-template <int MT, int NW>
+template <int MT, int NW, int UNI = -1>
 vbq_status launch_mv_nw(const MvArgs& a, int lds, hipStream_t s) {
-  const void* kernel = (const void*)vbq_mv_kernel<MT, NW>;
+  const void* kernel = (const void*)vbq_mv_kernel<MT, NW, UNI>;
   if (lds > 64 * 1024) {  // beyond the default dynamic LDS limit
     static std::atomic<uint64_t> done{0};
     vbq_status st = allow_big_lds(kernel, done);
@@ -1272,6 +1302,31 @@ vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
   a.M = M;
   a.S = sh.S;
   a.SW = sh.SW;
+  if constexpr (MT == 1) {
+    // a matrix of one width class (a "recipe" matrix) takes the uniform kernel
+    int uni = -1, classes = 0;
+    for (int c = 0; c < 4; ++c)
+      if (m.n_entries[c]) {
+        uni = c;
+        ++classes;
+      }
+    if (classes == 1) {
+      switch (uni * 3 + (sh.NW == 4 ? 0 : sh.NW == 8 ? 1 : 2)) {
+        case 0: return launch_mv_nw<1, 4, 0>(a, sh.lds, s);
+        case 1: return launch_mv_nw<1, 8, 0>(a, sh.lds, s);
+        case 2: return launch_mv_nw<1, 16, 0>(a, sh.lds, s);
+        case 3: return launch_mv_nw<1, 4, 1>(a, sh.lds, s);
+        case 4: return launch_mv_nw<1, 8, 1>(a, sh.lds, s);
+        case 5: return launch_mv_nw<1, 16, 1>(a, sh.lds, s);
+        case 6: return launch_mv_nw<1, 4, 2>(a, sh.lds, s);
+        case 7: return launch_mv_nw<1, 8, 2>(a, sh.lds, s);
+        case 8: return launch_mv_nw<1, 16, 2>(a, sh.lds, s);
+        case 9: return launch_mv_nw<1, 4, 3>(a, sh.lds, s);
+        case 10: return launch_mv_nw<1, 8, 3>(a, sh.lds, s);
+        default: return launch_mv_nw<1, 16, 3>(a, sh.lds, s);
+      }
+    }
+  }
   if (sh.NW == 4) return launch_mv_nw<MT, 4>(a, sh.lds, s);
   if constexpr (MT == 1) {
     if (sh.NW == 16) return launch_mv_nw<MT, 16>(a, sh.lds, s);

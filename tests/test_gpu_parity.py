@@ -113,6 +113,18 @@ def test_uniform_width_vs_dense_float32(vbq, bits_u):
     parity.check(yref32, ystar, rm, what="torch fp32 dense")
 
 
+@pytest.mark.parametrize("bits_u", [1, 2, 4, 8])
+@pytest.mark.parametrize("N,K,R,C", GEOMS)
+def test_uniform_width_gemv_all_geometries(vbq, bits_u, N, K, R, C):
+    """One-width matrices take the uniform kernel (no width map, positions from
+    ranks), including ragged tiles whose columns hold fewer than R rows."""
+    spec = synth.MatrixSpec("t", N % 5, bits_u, N, K, uniform_bits=bits_u)
+    bits, q, s = synth.make_matrix(spec, 103)
+    x = synth.make_x(spec, 103)[0]
+    y = _packed(vbq, q, s, bits, R, C).gemv(_x_dev(x)).cpu().numpy()
+    parity.check(y, omatmul.gemv(q, s, x), omatmul.row_magnitude(q, s, x), what=f"uniform {bits_u}")
+
+
 @pytest.mark.parametrize("M", [1, 2, 3, 4, 8, 11, 16])
 @pytest.mark.parametrize("N,K,R,C", [(257, 768, 16, 12), (130, 4096, 64, 64), (64, 14336, 16, 112)])
 def test_gemm_small_matches_oracle(vbq, M, N, K, R, C):
