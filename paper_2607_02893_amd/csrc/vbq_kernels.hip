@@ -221,6 +221,12 @@ __device__ __forceinline__ uint32_t lane_id_here() {
 }
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+// A wave-uniform value the compiler must treat as produced here (it cannot
+// hoist its uses above this point).
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  __asm__ __volatile__("" : "+s"(v));
+  return v;
+}
 
 // ---------------------------------------------------------------------------
 // Work split.  A workgroup of NW waves owns one row tile.  Each unit of the
@@ -644,10 +650,11 @@ struct XRegs {
 
 __device__ __forceinline__ void load_x1(const uint16_t* __restrict__ x, int j, int cols, XRegs& xr, uint32_t lane) {
   const int n = cols * 8;
+  const uint8_t* xb = (const uint8_t*)x;
 #pragma unroll
   for (int k = 0; k < kXRegs; ++k) {
     const int i = max(min((int)lane + 64 * k, n - 1), 0);
-    xr.v[k] = *(const u32x4*)(x + (size_t)(j + (i >> 3)) * 64 + (i & 7) * 8);
+    xr.v[k] = ld<u32x4>(xb, 128u * (uint32_t)j + 16u * (uint32_t)i);  // chunk i of the window
   }
 }
 
@@ -729,9 +736,17 @@ __device__ __forceinline__ void reduce_window(const Win& wn, int R, int cols, in
   }
 }
 
-// Start of unit `unit`'s class-c run in the class section.
+// Start of unit `unit`'s class-c run in the class section.  The unit table
+// is the blob's first section (offset 0, checked on the host).
 __device__ __forceinline__ uint32_t class_start(const DevMatrix& mat, int unit, int c) {
-  return ld<uint32_t>(mat.blob, mat.off_units + 4u * ((uint32_t)unit * vbq::kUnitRowWords + c));
+  return ld<uint32_t>(mat.blob, 4u * ((uint32_t)unit * vbq::kUnitRowWords + c));
+}
+// Rows `unit` and `unit` + 1 of the unit table (one 64-byte load; the table
+// has n_units + 1 rows): .s0123 are the unit's class-run starts, .s89ab the
+// next unit's.
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+__device__ __forceinline__ u32x16 unit_rows(const DevMatrix& mat, int unit) {
+  return ld<u32x16>(mat.blob, 4u * (uint32_t)unit * vbq::kUnitRowWords);
 }
 
 // Entries of a run that stay inside the class section (a malformed blob can
@@ -822,14 +837,41 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       lds_phase();
       continue;
     }
-    uint32_t ustart[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) ustart[c] = class_start(mat, unit, c);
+    // A whole-unit item (one slice per unit) reads where its class runs start
+    // and how long they are from the unit table (rows u and u + 1): no class
+    // counts, and its code loads do not wait for the width map.
+    const bool whole = MT == 1 && S == 1;  // wave-uniform
+    const u32x16 rows2 = unit_rows(mat, unit);
+    const u32x4 erow = rows2.s0123, enext = rows2.s89ab;
+    const uint32_t ustart[4] = {erow.x, erow.y, erow.z, erow.w};
     const WmapRegs wr = load_wmap(mat, u, slice_we, lane);
+    // The class sections' offsets and sizes come from the kernel-argument
+    // block (not preloaded): read them only now, so that the loads above do
+    // not wait for that block (it would otherwise be read, and waited for,
+    // before the work loop).
+    lds_phase();
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      mat.off_codes[c] = opaque(mat.off_codes[c]);
+      mat.off_scales[c] = opaque(mat.off_scales[c]);
+      mat.n_entries[c] = opaque(mat.n_entries[c]);
+    }
     auto window = [&](int c0, int c1) __attribute__((always_inline)) {
       const int cols = c1 - c0;
       const int wb = (c0 * R) >> 6, we = (c1 * R + 63) >> 6;
-      const WinCounts wc = window_counts(wr, u, wb, we, R, lane);
+      const bool unit_window = whole && c0 == cb && c1 == ce;  // wave-uniform
+      WinCounts wc;
+      if (unit_window) {
+        const u32x4 own = enext - erow;
+        wc.own[0] = own.x;
+        wc.own[1] = own.y;
+        wc.own[2] = own.z;
+        wc.own[3] = own.w;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) wc.before[c] = 0u;
+      } else {
+        wc = window_counts(wr, u, wb, we, R, lane);
+      }
       uint32_t start[4], seg[4];
       int n[4];
       uint32_t o = 0;
@@ -840,13 +882,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
         seg[c] = inv + 2u * o;
         o += wc.own[c];
       }
-      // one row: x arrived with the map, so it goes to LDS now, freeing its
-      // registers before the code batches are loaded
-      if constexpr (MT == 1) store_x1(cols, xr, wn, lane);
-      // the first batch of every class is in flight while the index is built
-      // (and, for several rows, x is staged): one memory latency for all four
-      // (several rows need the registers, and load the 8-bit one when its
-      // turn comes)
+      // the first batch of every class is in flight while x is stored and the
+      // index is built (and, for several rows, x is staged): one memory
+      // latency for all four (several rows need the registers, and load the
+      // 8-bit one when its turn comes)
       Batch<0, MT> A0;
       Batch<1, MT> A1;
       Batch<2, MT> A2;
@@ -855,6 +894,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       load_batch<1, MT>(A1, mat, start[1], n[1], 0, lane);
       load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
       if constexpr (MT == 1) load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
+      // one row: x arrived with the map and goes to LDS now
+      if constexpr (MT == 1) store_x1(cols, xr, wn, lane);
       build_index(wr, u, wb, we, R, wc, inv, lane);
       if constexpr (MT > 1) stage_x<MT>(a, u.j0 + c0, cols, wn, lane);
       lds_phase();
@@ -1176,8 +1217,10 @@ vbq_status make_dev_matrix(const vbq_desc* d, const void* blob, DevMatrix* m) {
   if (st != VBQ_OK) return st;
   if ((uintptr_t)blob % 256 != 0) return VBQ_ERR_BUFFER;
   if (d->total_bytes >= (1ull << 32)) return VBQ_ERR_UNSUPPORTED;  // 32-bit section offsets
+  // the kernels address the unit table at offset 0 (the layout's first section)
+  if (d->section_off[VBQ_SEC_UNITS] != 0) return VBQ_ERR_DESC;
   m->blob = (const uint8_t*)blob;
-  m->off_units = (uint32_t)d->section_off[VBQ_SEC_UNITS];
+  m->off_units = 0;
   m->off_wmap = (uint32_t)d->section_off[VBQ_SEC_WMAP];
   for (int c = 0; c < 4; ++c) {
     m->n_entries[c] = (uint32_t)d->n_entries[c];

@@ -53,9 +53,15 @@ inline vbq_status make_geometry(int64_t N, int64_t K, const vbq_pack_opts* o, Ge
   }
   if (!is_pow2(R) || R < 16 || R > 256) return VBQ_ERR_UNSUPPORTED;
   if (C == 0) {
-    int64_t cmax = kMaxUnitPositions / R < kMaxChunk ? kMaxUnitPositions / R : kMaxChunk;
-    int64_t U = ceil_div(g->G, cmax);
+    // one unit per wave of the one-row kernel: at least four units per tile,
+    // each at most 32 group columns wide, the count a multiple of four (a
+    // unit's entries of each class are one run of the unit table, so a wave
+    // that owns a whole unit needs no class counts of its own)
+    int64_t U = ceil_div(g->G, 32);
+    U = U < 4 ? 4 : (U + 3) / 4 * 4;
     C = (int32_t)ceil_div(g->G, U);
+    int64_t cmax = kMaxUnitPositions / R < kMaxChunk ? kMaxUnitPositions / R : kMaxChunk;
+    if (C > cmax) C = (int32_t)cmax;
   }
   if (C < 1 || C > kMaxChunk || (int64_t)R * C > kMaxUnitPositions) return VBQ_ERR_UNSUPPORTED;
   g->R = R;
