@@ -31,27 +31,37 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0
 METRIC = "fused dequant-GEMV effective HBM GB/s (% of peak) and µs per decode step"
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_02893_amd", "csrc", "vbq_kernels.hip")
+# the kernels and the packer's layout choices (tile and chunk sizes) decide the traffic
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_02893_amd", "csrc", f)
+                  for f in ("vbq_kernels.hip", "vbq_layout.hpp", "vbq_pack.cpp")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "vbq_mv_kernel_9b_step_traffic.md")
+TRAFFIC_CONFIG = "workload 3, M 1, widths mixed"  # the only configuration the counters were taken on
 CALIB_BYTES = 256 << 20  # plain copy used to scale the HBM byte counters
 
 
 def kernel_source_hash():
     import hashlib
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
-def measured_traffic():
+def measured_traffic(config):
     """HBM bytes per GEMV launch from the committed counter summary, or None
-    when that summary is missing or was taken on another kernel source."""
+    when that summary is missing, was taken on another kernel source, or on
+    another configuration than `config`."""
+    if config != TRAFFIC_CONFIG:
+        return None
     try:
         fields = {}
         with open(TRAFFIC_FILE) as f:
             for line in f:
                 if ":" in line and line.startswith("- "):
                     k, v = line[2:].split(":", 1)
-                    fields[k.strip()] = v.strip().strip("`")
+                    v = v.strip()
+                    fields[k.strip()] = v.split("`")[1] if v.startswith("`") else v
         if fields.get("kernel_source_sha256") != kernel_source_hash():
             return None
         return int(fields["hbm_bytes_per_launch"])
@@ -200,7 +210,8 @@ def write_traffic_file(path, summ):
         f"- fetch_bytes_per_launch: {summ['fetch_bytes_per_launch']:.0f}",
         f"- write_bytes_per_launch: {summ['write_bytes_per_launch']:.0f}",
         f"- hbm_bytes_per_launch: {summ['hbm_bytes_per_launch']}",
-        f"- kernel_source_sha256: `{summ['kernel_source_sha256']}`",
+        f"- kernel_source_sha256: `{summ['kernel_source_sha256']}` (vbq_kernels.hip, vbq_layout.hpp, "
+        "vbq_pack.cpp)",
         "",
         "bench.py reports hbm_bytes_per_launch as roofline.traffic while the kernel source still has this hash.",
     ]
@@ -220,6 +231,9 @@ def main():
     ap.add_argument("--workers", type=int, default=min(12, len(os.sched_getaffinity(0))))
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--cold", type=int, default=0, metavar="K",
+                    help="also time K steps one by one, each after a 1 GiB write that evicts L2 and the "
+                         "Infinity Cache (the write is outside the timed region)")
     ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 (eager launches only)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs of --profile (FETCH_SIZE, WRITE_SIZE) and exit")
@@ -344,8 +358,32 @@ def main():
     except Exception as e:  # graph capture is an optimisation of the same launches
         log(f"graph capture unavailable: {e}")
 
-    wall_s = graph_s if graph_s is not None else eager_s
-    gpu_s = graph_gpu_s if graph_gpu_s is not None else eager_gpu_s
+    # cold steps: every byte of the step comes from HBM (small workloads
+    # otherwise stay resident in the 256 MB Infinity Cache between steps)
+    cold_us = None
+    if args.cold > 0:
+        flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+        run1 = g.replay if graph_s is not None else step
+        ts = []
+        for _ in range(args.cold):
+            flush.fill_(1.0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            run1()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        del flush
+        torch.cuda.empty_cache()
+        cold_us = {"median": round(float(np.median(ts)), 2), "p10": round(float(np.percentile(ts, 10)), 2),
+                   "p90": round(float(np.percentile(ts, 90)), 2), "steps": args.cold}
+        log(f"cold: {cold_us['median']:.1f} us/step (median of {args.cold}, caches flushed before each)")
+
+    # the faster of the two timings of the same launches (a graph of one small
+    # kernel is bound by the graph launch itself)
+    use_graph = graph_s is not None and graph_s <= eager_s
+    wall_s = graph_s if use_graph else eager_s
+    gpu_s = graph_gpu_s if use_graph else eager_gpu_s
     # Every launch of the step is the same kernel and they run back to back,
     # so its average launch duration is the step's GPU time / launches.
     per_launch_s = gpu_s / len(mats)
@@ -398,7 +436,7 @@ def main():
             torch.cuda.synchronize()
             dense_s = (time.perf_counter() - t0) / nd
             dense = {"us_per_step": round(1e6 * dense_s, 1), "weight_bytes": 2 * total_w,
-                     "speedup_vbq": round(dense_s / (graph_s or eager_s), 2),
+                     "speedup_vbq": round(dense_s / min(eager_s, graph_s or eager_s), 2),
                      "note": "torch F.linear (fp16) over the dequantized weights, eager launches"}
             del ws
             torch.cuda.empty_cache()
@@ -406,7 +444,8 @@ def main():
         except Exception as e:
             log(f"dense baseline skipped: {e}")
 
-    traffic = measured_traffic()
+    traffic = measured_traffic(f"workload {args.workload}, M {M}, "
+                               f"widths {'uniform ' + str(args.uniform) if args.uniform else 'mixed'}")
     value = total_alg / wall_s / 1e9
     cpu = None
     if not args.no_cpu:
@@ -430,14 +469,15 @@ def main():
                                f"{total_w / 1e9:.2f}G weights", "M": M,
                    "uniform_bits": args.uniform or None,
                    "algorithmic_bytes_per_step": int(total_alg), "blob_bytes": int(blob_bytes),
-                   "timing": "HIP-graph replay of the step" if graph_s is not None else "eager launches"},
+                   "timing": "HIP-graph replay of the step" if use_graph else "eager launches"},
         "us_per_step": round(1e6 * wall_s, 2),
         "us_per_step_eager": round(1e6 * eager_s, 2),
         "us_per_step_graph": round(1e6 * graph_s, 2) if graph_s is not None else None,
+        "us_per_step_cold": cold_us,
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                     "kernel": f"vbq_mv_kernel<{1 if M == 1 else 2 if M == 2 else 4 if M <= 4 else 8 if M <= 8 else 16}>",
+                     "kernel": "vbq_mv_kernel<1>" if M == 1 else "vbq_mv_kernel<2>" if M == 2 else "vbq_mm_kernel",
                      "launches_per_step": len(mats),
                      "algorithmic_bytes_per_launch": round(alg_per_launch),
                      "avg_launch_us": round(1e6 * per_launch_s, 3),
