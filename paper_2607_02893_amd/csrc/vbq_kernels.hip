@@ -555,6 +555,10 @@ __device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits
   const int js = p >> wn.logR;
   // lane pairs of a half-entry class: the odd lane takes the high half
   const uint32_t xaddr = wn.xs + (uint32_t)__umul24((uint32_t)js, kXStride) + (L == 2 ? (lane & 1u) * 64u : 0u);
+  // the column sums first: their LDS latency overlaps the products
+  float Xm[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) Xm[m] = lds_f32(wn.Xs + 4u * (uint32_t)(m * wn.SW + js));
   float acc[MT][D::kSlots];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {  // local x chunk q holds pairs 4q..4q+3 of this lane's share
@@ -587,7 +591,7 @@ __device__ __forceinline__ void compute_entry(const uint32_t* w, uint16_t s_bits
 #pragma unroll
     for (int k = 1; k < D::kSlots; ++k) su = __builtin_fmaf(acc[m][k], D::inv_value(k), su);
     if constexpr (L == 2) su = add_dpp_f32_quad_xor1(su);  // both halves, the same sum in both lanes
-    const float X = lds_f32(wn.Xs + 4u * (uint32_t)(m * wn.SW + js));
+    const float X = Xm[m];
     const float sq = CLS == 0 ? __builtin_fmaf(su, 2.0f, -X) : __builtin_fmaf(-(float)(1 << (D::B - 1)), X, su);
     // (several rows: skipping the duplicates keeps the register allocator's
     // scheduling regions small; one row stores them, with no branch)
