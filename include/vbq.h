@@ -68,6 +68,10 @@
  *     are returned, a failed launch returns VBQ_ERR_HIP.
  *   - Device pointers must be 16-byte aligned; x / X are contiguous fp16.
  *   - Nothing throws across this interface.
+ *   - Environment: VBQ_ONE_WAVE_PER_UNIT=1 makes the one-row GEMV use one wave
+ *     per unit everywhere (by default small mixed-width matrices run two waves
+ *     per unit).  It exists to test both kernels on the same inputs; results
+ *     agree within the output tolerance, bitwise where both take whole units.
  */
 #ifndef VBQ_H
 #define VBQ_H

@@ -28,6 +28,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cstdlib>
 #include <cstdint>
 #include <type_traits>
 
@@ -932,6 +933,132 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
 }
 
 // ---------------------------------------------------------------------------
+// Two waves per unit (one activation row, mixed widths, small matrices).
+//
+// With one wave per unit a small matrix leaves each SIMD one or two waves,
+// and every wave runs its index build and its four class runs one after the
+// other, each a chain of LDS round trips.  Here a pair of waves shares the
+// unit: wave 2k loads the width map, builds the index and decodes the 1-bit
+// run; wave 2k + 1 loads x, stages it and decodes the 2-, 4- and 8-bit runs.
+// Both read the unit's class runs from the unit table (rows u and u + 1), so
+// both issue their first code loads at once.  Workgroup barriers separate
+// the set-up, the decode and the row reduction.
+// ---------------------------------------------------------------------------
+template <int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) void vbq_mv_pair_kernel(
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ blob, uint32_t off_wmap, uint32_t tile_words,
+    uint32_t chunk_words, uint32_t wmap_words, int32_t G, int32_t N, uint32_t geo, int32_t U, uint32_t sw_m,
+    MvArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  constexpr int NP = NW / 2;  // wave pairs: one unit each
+  DevMatrix mat = a.m;
+  mat.blob = blob;
+  mat.off_wmap = off_wmap;
+  mat.tile_words = tile_words;
+  mat.chunk_words = chunk_words;
+  mat.wmap_words = wmap_words;
+  mat.G = G;
+  mat.N = N;
+  mat.U = U;
+  mat.R = (int)(geo & 0x1FF);
+  mat.C = (int)((geo >> 9) & 0xFF);
+  mat.logR = (int)((geo >> 17) & 0xF);
+  const int R = mat.R, SW = (int)(sw_m & 0xFFFF);
+  const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
+  const uint32_t lane = lane_id();
+  const int wave = wave_id();
+  const int pair = wave >> 1, role = wave & 1;
+  const int t = blockIdx.x;
+  const WavePlan P = wave_plan(R, SW, 1);
+  const uint32_t ysum = lds0 + (uint32_t)(pair * R * 4);
+  const uint32_t region = lds0 + (uint32_t)(NP * R * 4 + pair * P.bytes);
+  Win wn;
+  wn.xs = region + P.xs;
+  wn.Xs = region + P.Xs;
+  wn.part = region + P.part;
+  wn.xstride_m = (uint32_t)(SW * kXStride);
+  wn.part_m = (uint32_t)(SW * R * 4);
+  wn.SW = SW;
+  wn.logR = mat.logR;
+  const uint32_t inv = region + P.inv;
+  if (role == 0)
+    for (int i = (int)lane; i < R; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
+
+  const bool active = pair < mat.U;  // wave-uniform
+  const UnitInfo u = load_unit(mat, t, active ? pair : 0);
+  const int unit = t * mat.U + (active ? pair : 0);
+  Batch<0, 1> A0;
+  Batch<1, 1> A1;
+  Batch<2, 1> A2;
+  Batch<3, 1> A3;
+  uint32_t start[4], seg[4];
+  int n[4];
+  if (active) {
+    WmapRegs wr;
+    XRegs xr;
+    if (role == 0)
+      wr = load_wmap(mat, u, u.W, lane);
+    else
+      load_x1(x, u.j0, u.cols, xr, lane);
+    const u32x16 rows2 = unit_rows(mat, unit);
+    const u32x4 erow = rows2.s0123, own = rows2.s89ab - rows2.s0123;
+    // (the class sections' offsets come from the kernel-argument block: read
+    // them only after the loads above are issued)
+    lds_phase();
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      mat.off_codes[c] = opaque(mat.off_codes[c]);
+      mat.off_scales[c] = opaque(mat.off_scales[c]);
+      mat.n_entries[c] = opaque(mat.n_entries[c]);
+    }
+    WinCounts wc;
+    wc.own[0] = own.x;
+    wc.own[1] = own.y;
+    wc.own[2] = own.z;
+    wc.own[3] = own.w;
+    const uint32_t es[4] = {erow.x, erow.y, erow.z, erow.w};
+    uint32_t o = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      wc.before[c] = 0u;
+      start[c] = es[c];
+      n[c] = clamp_run(mat, c, start[c], wc.own[c]);
+      seg[c] = inv + 2u * o;
+      o += wc.own[c];
+    }
+    if (role == 0) {
+      load_batch<0, 1>(A0, mat, start[0], n[0], 0, lane);
+      build_index(wr, u, 0, u.W, R, wc, inv, lane);
+    } else {
+      load_batch<1, 1>(A1, mat, start[1], n[1], 0, lane);
+      load_batch<2, 1>(A2, mat, start[2], n[2], 0, lane);
+      load_batch<3, 1>(A3, mat, start[3], n[3], 0, lane);
+      store_x1(u.cols, xr, wn, lane);
+    }
+  }
+  __syncthreads();  // the index and x of every unit are in LDS
+  if (active) {
+    if (role == 0) {
+      run_class<0, 1>(mat, A0, start[0], n[0], seg[0], wn, lane);
+    } else {
+      run_class<1, 1>(mat, A1, start[1], n[1], seg[1], wn, lane);
+      run_class<2, 1>(mat, A2, start[2], n[2], seg[2], wn, lane);
+      run_class<3, 1>(mat, A3, start[3], n[3], seg[3], wn, lane);
+    }
+  }
+  __syncthreads();  // every partial product is in LDS
+  if (active && role == 0) reduce_window<1>(wn, R, u.cols, u.rows, ysum, lane);
+  __syncthreads();
+  const int rows = min(R, mat.N - t * R);
+  for (int r = threadIdx.x; r < rows; r += NW * 64) {
+    float tot = 0.0f;
+#pragma unroll
+    for (int p2 = 0; p2 < NP; ++p2) tot += lds_f32(lds0 + 4u * (uint32_t)(p2 * R + r));
+    a.y[(size_t)t * R + r] = tot;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Several activation rows (3 <= M <= 16): matrix cores.
 //
 // Y[m][n] = sum_k w_hat[n][k] X[m][k] as 16 x 16 x 16 fp16 MFMA products
@@ -1336,8 +1463,66 @@ vbq_status launch_mv_nw(const MvArgs& a, int lds, hipStream_t s) {
   return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
 }
 
+// Wave pairs: one row, mixed widths, whole units of at most 32 columns, at
+// most 8 units per tile, and a grid small enough that one wave per unit would
+// leave the SIMDs with at most two waves each.
+constexpr int kPairMaxUnits = 2048;
+
+template <int NW>
+vbq_status launch_pair_nw(const MvArgs& a, int lds, hipStream_t s) {
+  const void* kernel = (const void*)vbq_mv_pair_kernel<NW>;
+  if (lds > 64 * 1024) {
+    static std::atomic<uint64_t> done{0};
+    vbq_status st = allow_big_lds(kernel, done);
+    if (st != VBQ_OK) return st;
+  }
+  MvArgs args = a;
+  const uint16_t* x = a.x;
+  const uint8_t* blob = a.m.blob;
+  uint32_t off_wmap = a.m.off_wmap, tile_words = a.m.tile_words, chunk_words = a.m.chunk_words;
+  uint32_t wmap_words = a.m.wmap_words;
+  int32_t G = a.m.G, N = a.m.N, U = a.m.U;
+  uint32_t geo = (uint32_t)a.m.R | ((uint32_t)a.m.C << 9) | ((uint32_t)a.m.logR << 17) | (1u << 21);
+  uint32_t sw_m = (uint32_t)a.SW | (1u << 16);
+  void* kargs[] = {&x, &blob, &off_wmap, &tile_words, &chunk_words, &wmap_words, &G, &N, &geo, &U, &sw_m, &args};
+  return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
+}
+
+// Launches the pair kernel when the matrix qualifies; *used says whether it did.
+vbq_status try_launch_pair(const DevMatrix& m, const void* x, float* y, hipStream_t s, bool* used) {
+  *used = false;
+  int classes = 0;
+  for (int c = 0; c < 4; ++c) classes += m.n_entries[c] ? 1 : 0;
+  if (classes < 2 || m.U < 2 || m.U > 8 || m.C > kXRegs * 8) return VBQ_OK;
+  if ((int64_t)m.T * m.U > kPairMaxUnits) return VBQ_OK;
+  const int NW = m.U <= 4 ? 8 : 16;
+  const int lds = (NW / 2) * (m.R * 4 + wave_plan(m.R, m.C, 1).bytes);
+  if (lds > kLdsLimit) return VBQ_OK;
+  MvArgs a;
+  a.m = m;
+  a.x = (const uint16_t*)x;
+  a.y = y;
+  a.ldx = m.K;
+  a.ldy = m.N;
+  a.M = 1;
+  a.S = 1;
+  a.SW = m.C;
+  *used = true;
+  return NW == 8 ? launch_pair_nw<8>(a, lds, s) : launch_pair_nw<16>(a, lds, s);
+}
+
 template <int MT>
 vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, float* y, int64_t ldy, hipStream_t s) {
+  if constexpr (MT == 1) {
+    // VBQ_ONE_WAVE_PER_UNIT=1 turns the pair kernel off (to test both paths
+    // on the same inputs)
+    const char* one = getenv("VBQ_ONE_WAVE_PER_UNIT");
+    if (!(one && one[0] == '1')) {
+      bool used = false;
+      const vbq_status st = try_launch_pair(m, x, y, s, &used);
+      if (used) return st;
+    }
+  }
   MvShape sh;
   if (!choose_shape(m, MT, &sh)) return VBQ_ERR_UNSUPPORTED;
   MvArgs a;

@@ -70,6 +70,35 @@ def test_gemv_matches_oracle(vbq, N, K, R, C):
     _say(f"  max rel err {rel:.2e}")
 
 
+# geometries the two-waves-per-unit kernel takes (mixed widths, 2..8 units
+# of at most 32 columns per tile, a small grid), with ragged tiles and units
+PAIR_GEOMS = [(6144, 4096, 0, 0), (4096, 14336, 0, 0), (1000, 4096, 0, 0), (37, 320, 0, 0), (17, 896, 0, 0),
+              (300, 640, 256, 3), (130, 1024, 32, 5), (77, 2048, 64, 11)]
+
+
+@pytest.mark.parametrize("N,K,R,C", PAIR_GEOMS)
+def test_pair_kernel_matches_one_wave_per_unit(vbq, N, K, R, C, monkeypatch):
+    """Both kernels match the oracle; where one wave per unit also takes whole
+    units (four or more units per tile) the two add the same per-unit row
+    sums in the same order, so their outputs are bitwise equal."""
+    _say(f"pair vs single N={N} K={K} R={R} C={C}")
+    spec = synth.MatrixSpec("t", N, K, N, K)
+    bits, q, s = synth.make_matrix(spec, 47)
+    x = synth.make_x(spec, 47)[0]
+    Wp = _packed(vbq, q, s, bits, R, C)
+    xd = _x_dev(x)
+    monkeypatch.delenv("VBQ_ONE_WAVE_PER_UNIT", raising=False)
+    y_pair = Wp.gemv(xd).cpu().numpy()
+    monkeypatch.setenv("VBQ_ONE_WAVE_PER_UNIT", "1")
+    y_one = Wp.gemv(xd).cpu().numpy()
+    monkeypatch.delenv("VBQ_ONE_WAVE_PER_UNIT")
+    if Wp.desc.n_chunks >= 4:
+        assert np.array_equal(y_pair, y_one)
+    want, mag = omatmul.gemv(q, s, x), omatmul.row_magnitude(q, s, x)
+    parity.check(y_pair, want, mag, what=f"pair gemv {N}x{K}")
+    parity.check(y_one, want, mag, what=f"one-wave gemv {N}x{K}")
+
+
 def test_one_hot_probe_is_exact(vbq):
     spec = synth.MatrixSpec("t", 0, 0, 300, 1024)
     bits, q, s = synth.make_matrix(spec, 47)
