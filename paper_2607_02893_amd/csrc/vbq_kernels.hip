@@ -637,6 +637,10 @@ __device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS, MT>& 
                                           uint32_t inv_c, const Win& wn, uint32_t lane) {
   constexpr int per_batch = Batch<CLS, MT>::E * Batch<CLS, MT>::G;
   const int nb = max(1, (n + per_batch - 1) / per_batch);
+  if (MT == 1 && nb == 1) {  // wave-uniform: no further batch, so no prefetch (each path keeps exact wait counts)
+    decode_batch<CLS, MT, kUni>(A, inv_c, n, 0, lane, wn);
+    return;
+  }
   Batch<CLS, MT> B;
   for (int b = 0; b < nb; b += 2) {
     load_batch<CLS, MT>(B, mat, start, n, min(b + 1, nb - 1), lane);
