@@ -62,7 +62,7 @@ def measured_traffic(config):
                     k, v = line[2:].split(":", 1)
                     v = v.strip()
                     fields[k.strip()] = v.split("`")[1] if v.startswith("`") else v
-        if fields.get("kernel_source_sha256") != kernel_source_hash():
+        if fields.get("kernel_source_sha256") != kernel_source_hash() or fields.get("config") != TRAFFIC_CONFIG:
             return None
         return int(fields["hbm_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
@@ -200,6 +200,7 @@ def write_traffic_file(path, summ):
         "",
         "(`$R` is the repository root.)  Per-launch figures, averaged over every GEMV launch of the step:",
         "",
+        f"- config: {TRAFFIC_CONFIG}",
         f"- launches: {summ['launches']}",
         f"- fetch_kib_per_launch_raw: {summ['fetch_kib_per_launch_raw']:.1f}",
         f"- write_kib_per_launch_raw: {summ['write_kib_per_launch_raw']:.1f}",
