@@ -71,7 +71,7 @@ def measured_traffic(config):
 
 def pmc_summary(fetch_dir, write_dir):
     """Summarise two rocprofv3 --pmc runs of `bench.py --profile` (FETCH_SIZE,
-    then WRITE_SIZE): per-launch KiB of the GEMV kernel, scaled by what the
+    then WRITE_SIZE): per-launch KiB of the GEMV kernels, scaled by what the
     same counters read for the calibration copy of CALIB_BYTES."""
     import csv
     import glob
@@ -83,7 +83,8 @@ def pmc_summary(fetch_dir, write_dir):
             if r["Counter_Name"] != counter:
                 continue
             name = r["Kernel_Name"]
-            key = "vbq" if "vbq_mv_kernel" in name else ("copy" if "MulFunctor" in name else None)
+            # every one-row GEMV kernel of the step (per-unit and two-waves-per-unit)
+            key = "vbq" if "vbq_mv_" in name else ("copy" if "MulFunctor" in name else None)
             if key is None:
                 continue
             acc.setdefault(key, {}).setdefault(r["Dispatch_Id"], 0.0)
@@ -478,7 +479,8 @@ def main():
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                     "kernel": "vbq_mv_kernel<1>" if M == 1 else "vbq_mv_kernel<2>" if M == 2 else "vbq_mm_kernel",
+                     "kernel": ("vbq_mv_kernel<1> / vbq_mv_pair_kernel (one-row GEMV)" if M == 1 else
+                                "vbq_mv_kernel<2>" if M == 2 else "vbq_mm_kernel"),
                      "launches_per_step": len(mats),
                      "algorithmic_bytes_per_launch": round(alg_per_launch),
                      "avg_launch_us": round(1e6 * per_launch_s, 3),
