@@ -118,18 +118,25 @@ def algorithmic_bytes(bits, N, K, M=1):
 
 
 def _gen_pack(task):
-    """Worker: draw one matrix and pack it with libvbq (host only)."""
+    """Worker: draw one matrix and pack it with libvbq (host only).  A matrix
+    with per-row widths (the recipe's tiered head) is packed as one row bucket
+    per width; every other matrix as one blob.  Returns its parts as
+    (output rows or None, blob, descriptor bytes, algorithmic bytes)."""
     idx, cfg, seed, spec = task
     from paper_2607_02893_amd import synth, vbq
     bits, q, s = synth.make_matrix(spec, seed)
-    blob, desc = vbq.pack_codes(q, s, bits, n_threads=1)
-    alg = algorithmic_bytes(bits, spec.N, spec.K)
-    return idx, np.asarray(blob).copy(), bytes(desc), alg, spec.N * spec.K
+    if spec.row_tiers is not None:
+        parts = [(rows, np.asarray(blob).copy(), bytes(d), algorithmic_bytes(bits[rows], len(rows), spec.K))
+                 for _, rows, blob, d in vbq.pack_row_buckets(q, s, bits, n_threads=1)]
+    else:
+        blob, desc = vbq.pack_codes(q, s, bits, n_threads=1)
+        parts = [(None, np.asarray(blob).copy(), bytes(desc), algorithmic_bytes(bits, spec.N, spec.K))]
+    return idx, parts, spec.N * spec.K
 
 
-def prepare(cfg, workers, uniform_bits=0):
+def prepare(cfg, workers, uniform_bits=0, recipe=False):
     from paper_2607_02893_amd import synth
-    wl = synth.workload(cfg, uniform_bits) if uniform_bits else synth.workload(cfg)
+    wl = synth.workload(cfg, uniform_bits, recipe=recipe)
     tasks = [(i, cfg, wl.seed, m) for i, m in enumerate(wl.matrices)]
     out = [None] * len(tasks)
     t0 = time.time()
@@ -230,6 +237,8 @@ def main():
     ap.add_argument("--batch", type=int, default=1, help="activation rows M (M > 1 times vbq_gemm_small)")
     ap.add_argument("--uniform", type=int, default=0, choices=(0, 1, 2, 4, 8),
                     help="every group of every matrix at this width (the 1.46B workload's roofline variants)")
+    ap.add_argument("--recipe", action="store_true",
+                    help="the deployed recipe's widths (one width per projection, the LM head as row buckets)")
     ap.add_argument("--workers", type=int, default=min(12, len(os.sched_getaffinity(0))))
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
@@ -252,7 +261,10 @@ def main():
               "(the row / K split that would shard it is described in the design notes).", file=sys.stderr)
         sys.exit(2)
 
-    wl, packed = prepare(args.workload, args.workers, args.uniform)
+    if args.recipe and (args.batch != 1 or args.uniform):
+        print("--recipe runs one activation row with the recipe's own widths", file=sys.stderr)
+        sys.exit(2)
+    wl, packed = prepare(args.workload, args.workers, args.uniform, args.recipe)
 
     import torch
     from paper_2607_02893_amd import synth, vbq
@@ -260,39 +272,50 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    mats = []
+    mats = []         # per matrix: ([(PackedMatrix, output rows or None)], x, y, algorithmic bytes)
+    launch_args = []  # per launch: (desc, blob, x, y, output-row map or 0, len(y))
+    launch_alg = []
     total_alg, total_w, blob_bytes = 0.0, 0, 0
-    for idx, blob, dbytes, alg, nw in packed:
-        desc = vbq.VbqDesc.from_buffer_copy(dbytes)
-        Wp = vbq.PackedMatrix(blob, desc, device=dev)
+    for idx, parts, nw in packed:
         spec = wl.matrices[idx]
         xm = synth.make_x(spec, wl.seed, args.batch)
         x = torch.from_numpy(np.ascontiguousarray(xm[0] if args.batch == 1 else xm)).to(dev)
         y = torch.empty(spec.N if args.batch == 1 else (args.batch, spec.N), dtype=torch.float32, device=dev)
-        alg += (2 * spec.K + 4 * spec.N) * (args.batch - 1)  # x and y of the extra rows
-        mats.append((Wp, x, y, alg))
+        dev_parts, alg = [], 0.0
+        for rows, blob, dbytes, palg in parts:
+            desc = vbq.VbqDesc.from_buffer_copy(dbytes)
+            Wp = vbq.PackedMatrix(blob, desc, device=dev)
+            rt = None if rows is None else torch.from_numpy(rows).to(dev)
+            dev_parts.append((Wp, rt))
+            palg += (2 * spec.K + 4 * desc.N) * (args.batch - 1)  # x and y of the extra rows
+            launch_args.append((desc, Wp.blob.data_ptr(), x.data_ptr(), y.data_ptr(),
+                                0 if rt is None else rt.data_ptr(), spec.N))
+            launch_alg.append(palg)
+            alg += palg
+            blob_bytes += desc.total_bytes
+        mats.append((dev_parts, x, y, alg))
         total_alg += alg
         total_w += nw
-        blob_bytes += desc.total_bytes
     del packed
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
-
-    launch_args = [(m[0].desc, m[0].blob.data_ptr(), m[1].data_ptr(), m[2].data_ptr()) for m in mats]
     M = args.batch
 
-    def launch(d, b, x, y, stream_ptr):
+    def launch(d, b, x, y, rows, ylen, stream_ptr):
+        if rows:
+            return vbq.raw_gemv_rows(d, b, x, y, ylen, rows, stream_ptr)
         if M == 1:
             return vbq.raw_gemv(d, b, x, y, stream_ptr)
         return vbq.raw_gemm_small(d, b, M, x, d.K, y, d.N, stream_ptr)
 
     def step():
-        for d, b, x, y in launch_args:
-            st = launch(d, b, x, y, sptr)
+        for la in launch_args:
+            st = launch(*la, sptr)
             if st != 0:
-                raise vbq.VbqError(st, "vbq_gemv / vbq_gemm_small")
+                raise vbq.VbqError(st, "vbq_gemv / vbq_gemv_rows / vbq_gemm_small")
 
-    log(f"{len(mats)} GEMVs, {total_w / 1e9:.2f}G weights, algorithmic {total_alg / 1e6:.1f} MB/step, "
+    log(f"{len(mats)} matrices in {len(launch_args)} launches, {total_w / 1e9:.2f}G weights, "
+        f"algorithmic {total_alg / 1e6:.1f} MB/step, "
         f"blobs {blob_bytes / 1e6:.1f} MB")
     for _ in range(args.warmup):
         step()
@@ -341,8 +364,8 @@ def main():
         with torch.cuda.stream(cap):
             csp = cap.cuda_stream
             g.capture_begin()
-            for d, b, x, y in launch_args:
-                st = launch(d, b, x, y, csp)
+            for la in launch_args:
+                st = launch(*la, csp)
                 if st != 0:
                     raise vbq.VbqError(st, "vbq_gemv (capture)")
             g.capture_end()
@@ -388,26 +411,27 @@ def main():
     gpu_s = graph_gpu_s if use_graph else eager_gpu_s
     # Every launch of the step is the same kernel and they run back to back,
     # so its average launch duration is the step's GPU time / launches.
-    per_launch_s = gpu_s / len(mats)
-    alg_per_launch = total_alg / len(mats)
+    n_launch = len(launch_args)
+    per_launch_s = gpu_s / n_launch
+    alg_per_launch = total_alg / n_launch
     achieved = alg_per_launch / per_launch_s / 1e9
 
     # per-matrix breakdown (diagnostic; each launch bracketed by its own events)
     n_ev = min(5, args.steps)
-    starts = [[torch.cuda.Event(enable_timing=True) for _ in mats] for _ in range(n_ev)]
-    ends = [[torch.cuda.Event(enable_timing=True) for _ in mats] for _ in range(n_ev)]
+    starts = [[torch.cuda.Event(enable_timing=True) for _ in launch_args] for _ in range(n_ev)]
+    ends = [[torch.cuda.Event(enable_timing=True) for _ in launch_args] for _ in range(n_ev)]
     for r in range(n_ev):
-        for i, (d, b, x, y) in enumerate(launch_args):
+        for i, la in enumerate(launch_args):
             starts[r][i].record(stream)
-            launch(d, b, x, y, sptr)
+            launch(*la, sptr)
             ends[r][i].record(stream)
     torch.cuda.synchronize()
-    dur = np.median(np.array([[starts[r][i].elapsed_time(ends[r][i]) * 1e-3 for i in range(len(mats))]
+    dur = np.median(np.array([[starts[r][i].elapsed_time(ends[r][i]) * 1e-3 for i in range(n_launch)]
                               for r in range(n_ev)]), axis=0)
     per_shape = {}
-    for i, (Wp, _, _, alg) in enumerate(mats):
-        key = f"{Wp.desc.N}x{Wp.desc.K}"
-        e = per_shape.setdefault(key, {"count": 0, "us": [], "alg_bytes": alg})
+    for i, la in enumerate(launch_args):
+        key = f"{la[0].N}x{la[0].K}" + (" (row bucket)" if la[4] else "")
+        e = per_shape.setdefault(key, {"count": 0, "us": [], "alg_bytes": launch_alg[i]})
         e["count"] += 1
         e["us"].append(1e6 * dur[i])
     per_shape = {k: {"count": v["count"], "us_median": round(float(np.median(v["us"])), 2),
@@ -420,8 +444,14 @@ def main():
     if not args.no_dense:
         try:
             ws = []
-            for Wp, x, y, _ in mats:
-                ws.append(Wp.dequant().half())
+            for parts, x, y, _ in mats:
+                if parts[0][1] is None:
+                    ws.append(parts[0][0].dequant().half())
+                else:  # row buckets: scatter each bucket's rows back into place
+                    w = torch.empty((y.shape[-1], parts[0][0].K), dtype=torch.float16, device=dev)
+                    for Wp, rows in parts:
+                        w[rows.long()] = Wp.dequant().half()
+                    ws.append(w)
             torch.cuda.synchronize()
             xs = [m[1].view(M, -1) for m in mats]
 
@@ -447,7 +477,7 @@ def main():
             log(f"dense baseline skipped: {e}")
 
     traffic = measured_traffic(f"workload {args.workload}, M {M}, "
-                               f"widths {'uniform ' + str(args.uniform) if args.uniform else 'mixed'}")
+                               f"widths {'recipe' if args.recipe else 'uniform ' + str(args.uniform) if args.uniform else 'mixed'}")
     value = total_alg / wall_s / 1e9
     cpu = None
     if not args.no_cpu:
@@ -467,9 +497,10 @@ def main():
         "dtype": "f32",
         "precision": "fp16 activations x {1,2,4,8}-bit codes with fp16 group scales, fp32 accumulation",
         "data": "synthetic (seeded draws; no trained weights)",
-        "config": {"workload": f"{wl.name} decode step (workload {args.workload}): {len(mats)} GEMVs, "
+        "config": {"workload": f"{wl.name} decode step (workload {args.workload}): {len(mats)} GEMVs"
+                               f"{f' in {n_launch} launches' if n_launch != len(mats) else ''}, "
                                f"{total_w / 1e9:.2f}G weights", "M": M,
-                   "uniform_bits": args.uniform or None,
+                   "uniform_bits": args.uniform or None, "recipe": bool(args.recipe),
                    "algorithmic_bytes_per_step": int(total_alg), "blob_bytes": int(blob_bytes),
                    "timing": "HIP-graph replay of the step" if use_graph else "eager launches"},
         "us_per_step": round(1e6 * wall_s, 2),
@@ -479,9 +510,10 @@ def main():
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                     "kernel": ("vbq_mv_kernel<1> / vbq_mv_pair_kernel (one-row GEMV)" if M == 1 else
+                     "kernel": ("vbq_mv_kernel<1, NW, width class> (one width; LM head as row buckets)" if args.recipe
+                                else "vbq_mv_kernel<1> / vbq_mv_pair_kernel (one-row GEMV)" if M == 1 else
                                 "vbq_mv_kernel<2>" if M == 2 else "vbq_mm_kernel"),
-                     "launches_per_step": len(mats),
+                     "launches_per_step": n_launch,
                      "algorithmic_bytes_per_launch": round(alg_per_launch),
                      "avg_launch_us": round(1e6 * per_launch_s, 3),
                      "timing": "HIP events on the launch stream around the timed region / launches",

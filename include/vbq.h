@@ -179,6 +179,19 @@ vbq_status vbq_desc_check(const vbq_desc* d);
 vbq_status vbq_gemv(const vbq_desc* desc, const void* blob_dev,
                     const void* x_dev, float* y_dev, void* stream);
 
+/* Row-bucketed output (paper section 6, "Fused kernels over packed weights":
+ * the mixed-precision LM head is stored as a few frequency-grouped row
+ * buckets; section 4, the recipe's frequency-tiered head).  As vbq_gemv, but
+ * row n of this matrix is written to y_dev[row_index_dev[n]]: a bucket is
+ * packed as its own matrix (one width, so no width map) and called with the
+ * output rows of its members.  row_index_dev: device int32[N]; an index
+ * outside [0, y_len) is not written (no error).  The caller owns every buffer;
+ * buckets of one output may run back to back on one stream.  Errors: NULL,
+ * SHAPE (y_len < 0), BUFFER (misaligned pointers), DESC, HIP. */
+vbq_status vbq_gemv_rows(const vbq_desc* desc, const void* blob_dev,
+                         const void* x_dev, float* y_dev, int64_t y_len,
+                         const int32_t* row_index_dev, void* stream);
+
 /* Y[m][n] = sum_k w_hat[n][k] * X[m][k] for m < M, 0 <= M <= 16
  * (small-batch decode).  X_dev: device fp16 rows with stride ldx >= K
  * elements (ldx % 8 == 0); Y_dev: device float32 rows with stride ldy >= N.

@@ -72,7 +72,21 @@ struct MvArgs {
   int32_t M;          // rows of x actually present (<= MT)
   int32_t S;          // slices per unit
   int32_t SW;         // group columns per window (LDS staging)
+  // one activation row only: output row n goes to y[rows[n]] (skipped unless
+  // 0 <= rows[n] < ylen); rows == nullptr writes y[n]
+  const int32_t* rows;
+  int64_t ylen;
 };
+
+// Stores output row n of a one-row product, through the row map if there is one.
+__device__ __forceinline__ void store_row(const MvArgs& a, size_t n, float v) {
+  if (a.rows == nullptr) {
+    a.y[n] = v;
+  } else {
+    const int64_t d = a.rows[n];
+    if (d >= 0 && d < a.ylen) a.y[d] = v;
+  }
+}
 
 __device__ __forceinline__ half2_t as_h2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
 
@@ -931,7 +945,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       float tot = 0.0f;
 #pragma unroll
       for (int w2 = 0; w2 < NW; ++w2) tot += lds_f32(lds0 + 4u * (uint32_t)(w2 * NS + slot));
-      a.y[m * a.ldy + (size_t)t * R + r] = tot;
+      if (MT == 1)
+        store_row(a, (size_t)t * R + r, tot);
+      else
+        a.y[m * a.ldy + (size_t)t * R + r] = tot;
     }
   }
 }
@@ -1058,7 +1075,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
     float tot = 0.0f;
 #pragma unroll
     for (int p2 = 0; p2 < NP; ++p2) tot += lds_f32(lds0 + 4u * (uint32_t)(p2 * R + r));
-    a.y[(size_t)t * R + r] = tot;
+    store_row(a, (size_t)t * R + r, tot);
   }
 }
 
@@ -1493,7 +1510,8 @@ vbq_status launch_pair_nw(const MvArgs& a, int lds, hipStream_t s) {
 }
 
 // Launches the pair kernel when the matrix qualifies; *used says whether it did.
-vbq_status try_launch_pair(const DevMatrix& m, const void* x, float* y, hipStream_t s, bool* used) {
+vbq_status try_launch_pair(const DevMatrix& m, const void* x, float* y, const int32_t* rows, int64_t ylen, hipStream_t s,
+                           bool* used) {
   *used = false;
   int classes = 0;
   for (int c = 0; c < 4; ++c) classes += m.n_entries[c] ? 1 : 0;
@@ -1511,19 +1529,22 @@ vbq_status try_launch_pair(const DevMatrix& m, const void* x, float* y, hipStrea
   a.M = 1;
   a.S = 1;
   a.SW = m.C;
+  a.rows = rows;
+  a.ylen = ylen;
   *used = true;
   return NW == 8 ? launch_pair_nw<8>(a, lds, s) : launch_pair_nw<16>(a, lds, s);
 }
 
 template <int MT>
-vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, float* y, int64_t ldy, hipStream_t s) {
+vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, float* y, int64_t ldy, hipStream_t s,
+                     const int32_t* rows = nullptr, int64_t ylen = 0) {
   if constexpr (MT == 1) {
     // VBQ_ONE_WAVE_PER_UNIT=1 turns the pair kernel off (to test both paths
     // on the same inputs)
     const char* one = getenv("VBQ_ONE_WAVE_PER_UNIT");
     if (!(one && one[0] == '1')) {
       bool used = false;
-      const vbq_status st = try_launch_pair(m, x, y, s, &used);
+      const vbq_status st = try_launch_pair(m, x, y, rows, ylen, s, &used);
       if (used) return st;
     }
   }
@@ -1538,6 +1559,8 @@ vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
   a.M = M;
   a.S = sh.S;
   a.SW = sh.SW;
+  a.rows = MT == 1 ? rows : nullptr;
+  a.ylen = ylen;
   if constexpr (MT == 1) {
     // a matrix of one width class (a "recipe" matrix) takes the uniform kernel
     int uni = -1, classes = 0;
@@ -1632,6 +1655,17 @@ vbq_status vbq_gemv(const vbq_desc* desc, const void* blob_dev, const void* x_de
   if (st != VBQ_OK) return st;
   if ((uintptr_t)x_dev % 16 || (uintptr_t)y_dev % 4) return VBQ_ERR_BUFFER;
   return launch_mv<1>(m, x_dev, desc->K, 1, y_dev, desc->N, (hipStream_t)stream);
+}
+
+vbq_status vbq_gemv_rows(const vbq_desc* desc, const void* blob_dev, const void* x_dev, float* y_dev, int64_t y_len,
+                         const int32_t* row_index_dev, void* stream) {
+  if (!x_dev || !y_dev || !row_index_dev) return VBQ_ERR_NULL;
+  if (y_len < 0) return VBQ_ERR_SHAPE;
+  DevMatrix m;
+  vbq_status st = make_dev_matrix(desc, blob_dev, &m);
+  if (st != VBQ_OK) return st;
+  if ((uintptr_t)x_dev % 16 || (uintptr_t)y_dev % 4 || (uintptr_t)row_index_dev % 4) return VBQ_ERR_BUFFER;
+  return launch_mv<1>(m, x_dev, desc->K, 1, y_dev, desc->N, (hipStream_t)stream, row_index_dev, y_len);
 }
 
 vbq_status vbq_gemm_small(const vbq_desc* desc, const void* blob_dev, int64_t M, const void* X_dev, int64_t ldx,

@@ -16,6 +16,13 @@ used):
   * levels: uniform over the level set of the group's width,
     {-(2^(b-1)-1) .. 2^(b-1)-1} for b >= 2 and {-1, +1} for b = 1;
   * activations: N(0, 1) rounded to fp16, from key (layer, proj, 1000 + m).
+
+Recipe variant (paper section 4, the fixed recipe that is deployed): the
+first block's MLP (gate, up, down) at 4 bits, every other projection at
+2 bits, and the LM head tiered per row by token-frequency rank -- top 0.5% of
+rows at 8 bits, the next 1.5% at 4, the next 10% at 2, the rest at 1 (mean
+1.18 bits).  No corpus is available, so a row's rank is a seeded random
+permutation of the vocabulary (key (layer, proj, 2000)).
 """
 
 from dataclasses import dataclass, field
@@ -25,6 +32,8 @@ import numpy as np
 G = 64
 MIX_PILOT = {1: 0.69, 2: 0.15, 4: 0.12, 8: 0.04}       # mean 1.79 bits
 MIX_FIRST_MLP = {1: 0.30, 2: 0.50, 4: 0.10, 8: 0.10}   # mean 2.50 bits
+# recipe head: (fraction of rows by frequency rank, bits), most frequent first
+RECIPE_HEAD_TIERS = ((0.005, 8), (0.015, 4), (0.10, 2), (0.88, 1))
 WIDTHS = (1, 2, 4, 8)
 
 
@@ -91,6 +100,7 @@ class MatrixSpec:
     row_mix: dict = None          # per-row widths on a random subset of rows
     row_mix_rows: float = 0.0     # fraction of rows that take row_mix
     uniform_bits: int = 0         # 1/2/4/8: every group has this width
+    row_tiers: tuple = None       # ((fraction, bits), ...): per-row widths by frequency rank
 
     @property
     def groups(self):
@@ -106,28 +116,31 @@ class Workload:
 
 
 def _decoder(name, seed, d, layers, mlp, vocab, kv=None, first_mlp_mix=None,
-             head=None, uniform_bits=0):
+             head=None, uniform_bits=0, recipe=False):
     """Decode-step matrices in call order.  Projections that read the same
-    input are stored as one row-concatenated matrix: Q|K|V and gate|up."""
+    input are stored as one row-concatenated matrix: Q|K|V and gate|up.
+    recipe: the deployed recipe's widths (module docstring)."""
     kv = d if kv is None else kv
     mats = []
     for layer in range(layers):
         mlp_mix = first_mlp_mix if (layer == 0 and first_mlp_mix) else MIX_PILOT
-        mats.append(MatrixSpec("qkv", layer, 0, d + 2 * kv, d, uniform_bits=uniform_bits))
-        mats.append(MatrixSpec("o", layer, 1, d, d, uniform_bits=uniform_bits))
-        mats.append(MatrixSpec("gate_up", layer, 2, 2 * mlp, d, mix=dict(mlp_mix),
-                               uniform_bits=uniform_bits))
-        mats.append(MatrixSpec("down", layer, 3, d, mlp, mix=dict(mlp_mix),
-                               uniform_bits=uniform_bits))
-    hs = MatrixSpec("head", layers, 4, vocab, d, uniform_bits=uniform_bits)
-    if head is not None:
+        attn_u = 2 if recipe else uniform_bits
+        mlp_u = (4 if layer == 0 else 2) if recipe else uniform_bits
+        mats.append(MatrixSpec("qkv", layer, 0, d + 2 * kv, d, uniform_bits=attn_u))
+        mats.append(MatrixSpec("o", layer, 1, d, d, uniform_bits=attn_u))
+        mats.append(MatrixSpec("gate_up", layer, 2, 2 * mlp, d, mix=dict(mlp_mix), uniform_bits=mlp_u))
+        mats.append(MatrixSpec("down", layer, 3, d, mlp, mix=dict(mlp_mix), uniform_bits=mlp_u))
+    hs = MatrixSpec("head", layers, 4, vocab, d, uniform_bits=0 if recipe else uniform_bits)
+    if recipe:
+        hs.row_tiers = RECIPE_HEAD_TIERS
+    elif head is not None:
         for k, v in head.items():
             setattr(hs, k, v)
     mats.append(hs)
     return Workload(name, seed, mats)
 
 
-def workload(cfg, uniform_bits=0):
+def workload(cfg, uniform_bits=0, recipe=False):
     """The five synthetic decode workloads, by index.
 
     0: one 512x512 GEMV, mix of the adaptive pilot.
@@ -139,7 +152,16 @@ def workload(cfg, uniform_bits=0):
        vocab 128256.
     4: 1.46B-class shapes: d=2048, 32 layers, MLP 8192, vocab 50304,
        batch M in {1,2,4,8,16}; uniform_bits selects the uniform variants.
+    recipe=True (workloads 2, 3, 4): the same shapes with the deployed
+    recipe's widths instead of the per-group mixes.
     """
+    if recipe:
+        if cfg not in (2, 3, 4):
+            raise ValueError("the recipe variant exists for the decoder workloads 2, 3 and 4")
+        shapes = {2: ("1.0B-class", 2048, 24, 8192, 50304, None), 3: ("9B-class", 4096, 32, 14336, 128256, 1024),
+                  4: ("1.46B-class", 2048, 32, 8192, 50304, None)}[cfg]
+        name, d, layers, mlp, vocab, kv = shapes
+        return _decoder(name + "-recipe", 20260750 + cfg, d, layers, mlp, vocab, kv=kv, recipe=True)
     if cfg == 0:
         return Workload("gemv-512x512", 20260700, [MatrixSpec("w", 0, 0, 512, 512)])
     if cfg == 1:
@@ -159,10 +181,27 @@ def workload(cfg, uniform_bits=0):
     raise ValueError(f"no workload {cfg}")
 
 
+def tier_widths(N, tiers, rng):
+    """Per-row widths uint8[N] for frequency tiers ((fraction, bits), ...):
+    rows are ranked by a random permutation (rank 0 = most frequent) and the
+    tiers take consecutive rank ranges, the last one the remainder."""
+    rank_to_row = rng.permutation(N)
+    w = np.empty(N, dtype=np.uint8)
+    lo = 0
+    for i, (frac, b) in enumerate(tiers):
+        hi = N if i == len(tiers) - 1 else min(N, lo + int(round(frac * N)))
+        w[rank_to_row[lo:hi]] = b
+        lo = hi
+    return w
+
+
 def make_bits(spec, seed):
     rng = rng_for(seed, spec.layer, spec.proj)
     Gc = spec.K // G
-    if spec.uniform_bits:
+    if spec.row_tiers is not None:
+        w = tier_widths(spec.N, spec.row_tiers, rng_for(seed, spec.layer, spec.proj, 2000))
+        bits = np.repeat(w[:, None], Gc, axis=1)
+    elif spec.uniform_bits:
         bits = np.full((spec.N, Gc), spec.uniform_bits, dtype=np.uint8)
     else:
         bits = draw_bits(rng, spec.N, Gc, spec.mix)

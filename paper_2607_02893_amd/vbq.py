@@ -55,7 +55,7 @@ STATUS = {0: "VBQ_OK", 1: "VBQ_ERR_NULL", 2: "VBQ_ERR_SHAPE", 3: "VBQ_ERR_BITS",
           9: "VBQ_ERR_HIP", 10: "VBQ_ERR_UNSUPPORTED"}
 # exported symbols, in the order include/vbq.h declares them
 EXPORTS = ("vbq_status_string", "vbq_last_hip_error", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
-           "vbq_desc_check", "vbq_gemv", "vbq_gemm_small", "vbq_dequant")
+           "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_gemm_small", "vbq_dequant")
 
 
 class VbqDesc(ctypes.Structure):
@@ -101,6 +101,8 @@ _lib.vbq_desc_check.restype = ctypes.c_int
 _lib.vbq_desc_check.argtypes = [ctypes.POINTER(VbqDesc)]
 _lib.vbq_gemv.restype = ctypes.c_int
 _lib.vbq_gemv.argtypes = [ctypes.POINTER(VbqDesc), _P, _P, _P, _P]
+_lib.vbq_gemv_rows.restype = ctypes.c_int
+_lib.vbq_gemv_rows.argtypes = [ctypes.POINTER(VbqDesc), _P, _P, _P, ctypes.c_int64, _P, _P]
 _lib.vbq_gemm_small.restype = ctypes.c_int
 _lib.vbq_gemm_small.argtypes = [ctypes.POINTER(VbqDesc), _P, ctypes.c_int64, _P, ctypes.c_int64, _P,
                                 ctypes.c_int64, _P]
@@ -184,6 +186,26 @@ def pack_codes(q, scales, bits, tile_rows=0, chunk_groups=0, n_threads=0):
     return blob, d
 
 
+def pack_row_buckets(q, scales, bits, tile_rows=0, chunk_groups=0, n_threads=0):
+    """Pack a matrix whose rows each have one width (a recipe head: paper section
+    4, frequency-tiered rows; section 6, stored as frequency-grouped row buckets)
+    as one packed matrix per width.  Returns [(width, rows, blob, desc)] in
+    increasing width, rows the int32 output rows of the bucket's members in
+    order.  Each bucket has one width, so it carries no width map."""
+    q = np.ascontiguousarray(q, dtype=np.int8)
+    scales = np.ascontiguousarray(scales, dtype=np.uint16)
+    bits = np.ascontiguousarray(bits, dtype=np.uint8)
+    w = bits[:, 0]
+    if not np.array_equal(bits, np.repeat(w[:, None], bits.shape[1], axis=1)):
+        raise ValueError("row buckets need one width per row")
+    out = []
+    for b in np.unique(w):
+        rows = np.nonzero(w == b)[0].astype(np.int32)
+        blob, d = pack_codes(q[rows], scales[rows], bits[rows], tile_rows, chunk_groups, n_threads)
+        out.append((int(b), rows, blob, d))
+    return out
+
+
 def desc_check(d):
     return _lib.vbq_desc_check(ctypes.byref(d))
 
@@ -225,6 +247,21 @@ class PackedMatrix:
                              _stream_handle(stream)), "vbq_gemv")
         return y
 
+    def gemv_rows(self, x, y, rows, stream=None):
+        """y[rows[n]] = (w_hat @ x)[n] for every n (indices outside y are not written): one row
+        bucket of a bucketed matrix.  y: float32 device tensor; rows: int32 device tensor of length N."""
+        import torch
+        if x.dtype != torch.float16 or not x.is_contiguous() or x.numel() != self.K:
+            raise ValueError("x must be a contiguous float16 tensor of length K")
+        if y.dtype != torch.float32 or not y.is_contiguous():
+            raise ValueError("y must be a contiguous float32 tensor")
+        if rows.dtype != torch.int32 or not rows.is_contiguous() or rows.numel() != self.N:
+            raise ValueError("rows must be a contiguous int32 tensor of length N")
+        _check(_lib.vbq_gemv_rows(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()),
+                                  ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()), y.numel(),
+                                  ctypes.c_void_p(rows.data_ptr()), _stream_handle(stream)), "vbq_gemv_rows")
+        return y
+
     def gemm_small(self, X, Y=None, stream=None):
         """Y[M][N] (float32) = X @ w_hat^T for an fp16 device tensor X[M][K], M <= 16."""
         import torch
@@ -248,10 +285,42 @@ class PackedMatrix:
         return W
 
 
+class BucketedMatrix:
+    """A row-bucketed matrix in device memory: one PackedMatrix per width and
+    the output rows of its members (see pack_row_buckets)."""
+
+    def __init__(self, buckets, N, K, device="cuda"):
+        import torch
+        self.N, self.K = N, K
+        self.parts = [(b, PackedMatrix(blob, d, device), torch.from_numpy(rows).to(device))
+                      for b, rows, blob, d in buckets]
+        if sum(p[1].N for p in self.parts) != N:
+            raise ValueError("the buckets must hold every row once")
+
+    @property
+    def nbytes(self):
+        return sum(p[1].nbytes for p in self.parts)
+
+    def gemv(self, x, y=None, stream=None):
+        """y[N] (float32) = w_hat @ x: one vbq_gemv_rows per bucket, on one stream."""
+        import torch
+        if y is None:
+            y = torch.empty(self.N, dtype=torch.float32, device=x.device)
+        for _, Wp, rows in self.parts:
+            Wp.gemv_rows(x, y, rows, stream)
+        return y
+
+
 def raw_gemv(desc, blob_ptr, x_ptr, y_ptr, stream_ptr):
     """vbq_gemv on raw device addresses (no checks beyond the library's own)."""
     return _lib.vbq_gemv(ctypes.byref(desc), ctypes.c_void_p(blob_ptr), ctypes.c_void_p(x_ptr),
                          ctypes.c_void_p(y_ptr), ctypes.c_void_p(stream_ptr))
+
+
+def raw_gemv_rows(desc, blob_ptr, x_ptr, y_ptr, y_len, rows_ptr, stream_ptr):
+    """vbq_gemv_rows on raw device addresses."""
+    return _lib.vbq_gemv_rows(ctypes.byref(desc), ctypes.c_void_p(blob_ptr), ctypes.c_void_p(x_ptr),
+                              ctypes.c_void_p(y_ptr), y_len, ctypes.c_void_p(rows_ptr), ctypes.c_void_p(stream_ptr))
 
 
 def raw_gemm_small(desc, blob_ptr, M, X_ptr, ldx, Y_ptr, ldy, stream_ptr):

@@ -295,3 +295,70 @@ def test_workload4_uniform_variants(vbq, ub):
     for spec in (wl.matrices[2], wl.matrices[-1]):
         w = _sampled_check(vbq, spec, wl.seed)
         _say(f"cfg4 u{ub} {spec.name} {spec.N}x{spec.K}: max rel err {w:.2e}")
+
+
+# ------------------------------------------------------------------ recipe mode
+
+def test_gemv_rows_index_map(vbq):
+    """vbq_gemv_rows writes row n to y[rows[n]] with the same value vbq_gemv
+    gives (same kernel, same order: bitwise), skips indices outside y and
+    leaves every other entry of y alone."""
+    spec = synth.MatrixSpec("t", 0, 0, 500, 1024)
+    bits, q, s = synth.make_matrix(spec, 79)
+    Wp = _packed(vbq, q, s, bits)
+    xd = _x_dev(synth.make_x(spec, 79)[0])
+    y_ref = Wp.gemv(xd).cpu().numpy()
+    ylen = 1200
+    rows = synth.rng_for(79, 3).permutation(ylen)[:spec.N].astype(np.int32)
+    rows[[3, 77, 499]] = [-1, ylen, 1 << 30]  # not written
+    y = torch.full((ylen,), -7.0, dtype=torch.float32, device="cuda")
+    Wp.gemv_rows(xd, y, torch.from_numpy(rows).cuda())
+    y = y.cpu().numpy()
+    ok = (rows >= 0) & (rows < ylen)
+    assert np.array_equal(y[rows[ok]], y_ref[ok])
+    untouched = np.ones(ylen, dtype=bool)
+    untouched[rows[ok]] = False
+    assert np.all(y[untouched] == -7.0)
+
+
+@pytest.mark.parametrize("N,K", [(3000, 1024), (700, 4096), (100, 640)])
+def test_row_buckets_match_oracle(vbq, N, K):
+    """A frequency-tiered head (the recipe's 8/4/2/1-bit rows) packed as four
+    one-width row buckets: the bucketed product matches the oracle, and the
+    same matrix packed whole (width map, mixed-width kernel) within the same
+    tolerance."""
+    _say(f"row buckets N={N} K={K}")
+    spec = synth.MatrixSpec("h", 0, 4, N, K, row_tiers=synth.RECIPE_HEAD_TIERS)
+    bits, q, s = synth.make_matrix(spec, 83)
+    x = synth.make_x(spec, 83)[0]
+    xd = _x_dev(x)
+    Wb = vbq.BucketedMatrix(vbq.pack_row_buckets(q, s, bits), N, K)
+    y_b = Wb.gemv(xd).cpu().numpy()
+    y_w = _packed(vbq, q, s, bits).gemv(xd).cpu().numpy()
+    want, mag = omatmul.gemv(q, s, x), omatmul.row_magnitude(q, s, x)
+    rel = parity.check(y_b, want, mag, what=f"bucketed {N}x{K}")
+    parity.check(y_w, want, mag, what=f"whole {N}x{K}")
+    _say(f"  max rel err {rel:.2e}")
+
+
+def test_recipe_workload_full_size(vbq):
+    """The 9B-class recipe step at full size: uniform 2- and 4-bit projections
+    (the one-width kernel) and the tiered LM head as row buckets, sampled rows
+    against the oracle."""
+    wl = synth.workload(3, recipe=True)
+    picks = [m for m in wl.matrices if m.layer == 0] + [m for m in wl.matrices if m.layer == 1 and m.proj == 3]
+    for spec in picks:
+        w = _sampled_check(vbq, spec, wl.seed)
+        _say(f"recipe {spec.name} L{spec.layer} {spec.N}x{spec.K}: max rel err {w:.2e}")
+    head = wl.matrices[-1]
+    bits, q, s = synth.make_matrix(head, wl.seed)
+    x = synth.make_x(head, wl.seed)[0]
+    Wb = vbq.BucketedMatrix(vbq.pack_row_buckets(q, s, bits), head.N, head.K)
+    y = Wb.gemv(_x_dev(x)).cpu().numpy()
+    w = bits[:, 0]
+    rows = np.unique(np.concatenate([np.nonzero(w == b)[0][:24] for b in (1, 2, 4, 8)] +
+                                    [synth.rng_for(wl.seed, 9).choice(head.N, size=160, replace=False)]))
+    rel = parity.check(y[rows], omatmul.gemv(q[rows], s[rows], x), omatmul.row_magnitude(q[rows], s[rows], x),
+                       what="recipe head")
+    assert np.all(np.isfinite(y))
+    _say(f"recipe head {head.N}x{head.K} (4 buckets): max rel err {rel:.2e}")

@@ -203,3 +203,52 @@ def test_null_and_buffer_errors():
 def test_single_hip_runtime():
     """libvbq must share torch's HIP runtime: one libamdhip64 in the process."""
     assert len(vbq.hip_runtimes()) == 1
+
+
+# ------------------------------------------------------------------ recipe mode
+
+def test_recipe_workload_widths():
+    """The recipe variant (paper section 4): layer-0 MLP at 4 bits, every other
+    projection at 2 bits, the head tiered 0.5 / 1.5 / 10 / 88 % of rows at
+    8 / 4 / 2 / 1 bits (mean 1.18 bits per weight)."""
+    wl = synth.workload(4, recipe=True)
+    for spec in wl.matrices[:-1]:
+        bits, _ = synth.make_bits(spec, wl.seed)
+        want = 4 if (spec.layer == 0 and spec.name in ("gate_up", "down")) else 2
+        assert np.all(bits == want), (spec.name, spec.layer)
+    head = wl.matrices[-1]
+    bits, _ = synth.make_bits(head, wl.seed)
+    w = bits[:, 0]
+    assert np.all(bits == w[:, None])
+    N = head.N
+    counts = {b: int(np.count_nonzero(w == b)) for b in (1, 2, 4, 8)}
+    assert counts[8] == round(0.005 * N) and counts[4] == round(0.015 * N) and counts[2] == round(0.10 * N)
+    assert sum(counts.values()) == N
+    assert abs(w.mean() - 1.18) < 0.005
+    # the tiers are not contiguous row ranges (a frequency rank is not the row order)
+    assert np.any(np.diff(np.nonzero(w == 8)[0]) > 1)
+
+
+def test_pack_row_buckets_partition_and_bytes():
+    """One packed matrix per width: the buckets partition the rows in order,
+    each bucket has one width (no width-map words beyond its geometry's zero
+    planes) and its bytes equal the oracle's packer on the same rows."""
+    spec = synth.MatrixSpec("h", 0, 4, 777, 640, row_tiers=synth.RECIPE_HEAD_TIERS)
+    bits, q, s = synth.make_matrix(spec, 71)
+    bk = vbq.pack_row_buckets(q, s, bits)
+    rows_all = np.sort(np.concatenate([r for _, r, _, _ in bk]))
+    assert np.array_equal(rows_all, np.arange(spec.N))
+    for b, rows, blob, d in bk:
+        assert rows.dtype == np.int32 and np.all(np.diff(rows) > 0)
+        assert np.all(bits[rows] == b)
+        c = {1: 0, 2: 1, 4: 2, 8: 3}[b]
+        assert d.n_entries[c] == len(rows) * (spec.K // 64) and sum(d.n_entries) == d.n_entries[c]
+        ob, _ = olayout.pack(q[rows], s[rows], bits[rows], d.tile_rows, d.chunk_groups)
+        assert np.array_equal(np.asarray(ob), np.asarray(blob))
+
+
+def test_pack_row_buckets_rejects_mixed_rows():
+    spec = synth.MatrixSpec("t", 0, 0, 40, 256)
+    bits, q, s = synth.make_matrix(spec, 73)  # per-group widths
+    with pytest.raises(ValueError):
+        vbq.pack_row_buckets(q, s, bits)
