@@ -17,6 +17,10 @@ Modules
               fused kernels must reproduce (paper section 6).
   storage  -- packed-storage accounting, params * mean_bits / 8 (paper
               section 4, "Training", and Table 1).
+  qat      -- differentiable bit selection: the Gumbel-Softmax mix of the four
+              candidate reconstructions, the expected bit cost, the hardened
+              widths and the logit-step gradient (paper sections 3.2-3.3 and
+              Algorithm 1).
 
 Readings of the paper that the oracle fixes (every one is listed, with its
 justification, in the design notes of the repository):
@@ -33,6 +37,6 @@ method fixes (hand-computed groups from Eq. (1), closed forms, invariants,
 brute force on tiny inputs); none is "parity unpinned".
 """
 
-from . import quant, layout, matmul, storage  # noqa: F401
+from . import quant, layout, matmul, storage, qat  # noqa: F401
 
-__all__ = ["quant", "layout", "matmul", "storage"]
+__all__ = ["quant", "layout", "matmul", "storage", "qat"]
