@@ -15,6 +15,9 @@
  *     the group scale and accumulates the matrix-vector product; the
  *     full-precision matrix is never materialised (paper section 6, "Fused
  *     kernels over packed weights").
+ *   - Training chooses the widths (paper section 3.2, Algorithm 1): each group
+ *     mixes its four candidate reconstructions with Gumbel-Softmax weights;
+ *     vbq_qat_forward computes that mix (last part of this header).
  *
  * Readings fixed by this library where the paper is silent:
  *   - round() is round-half-to-even; the codes are computed against the scale
@@ -204,6 +207,64 @@ vbq_status vbq_gemm_small(const vbq_desc* desc, const void* blob_dev,
  * For checking the packed stream against the quantizer bit for bit. */
 vbq_status vbq_dequant(const vbq_desc* desc, const void* blob_dev,
                        float* W_dev, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Differentiable bit selection (training time; paper section 3.2 and
+ * Algorithm 1).  These calls work on plain (unpacked) fp32 weights seen as a
+ * flat array of n_groups groups of 64 contiguous weights: a row-major W[N][K]
+ * with K % 64 == 0 is n_groups = N*K/64, and the concatenation of several such
+ * matrices (a network's flat parameter buffer) can be passed as one array.
+ * Candidate order everywhere is B = {1, 2, 4, 8} bits.
+ * ------------------------------------------------------------------------- */
+
+#define VBQ_QAT_MAX_GROUPS (((int64_t)1) << 40)
+
+/* Bytes of device workspace vbq_qat_forward needs to compute bbar for
+ * n_groups groups (8 bytes per block of its launch).  VBQ_ERR_NULL or
+ * VBQ_ERR_SHAPE (n_groups < 0 or > VBQ_QAT_MAX_GROUPS). */
+vbq_status vbq_qat_workspace_size(int64_t n_groups, size_t* bytes);
+
+/* Forward pass of the selection path (paper section 3.2, Algorithm 1 lines of
+ * the weight and logit steps that build w_hat).  For each group g:
+ *   w_hat^(b)  = the per-group quantizer of section 3.1 at width b, exactly as
+ *                vbq_pack applies it (Eq. (1) for b >= 2, sign/absmean for
+ *                b = 1, fp16-rounded scale, round-half-to-even against the
+ *                stored scale, sign(0) = +1), so a one-hot pi gives exactly the
+ *                weights vbq_dequant returns after vbq_pack at that width;
+ *   pi_g       = softmax((logits_g + noise_g) / tau) in fp32;
+ *   w_soft_i   = sum_k pi_{g,k} * w_hat^(B_k)_i (fp32, FMA);
+ *   hard_g     = B[argmax_k logits_{g,k}] (first of equal maxima; the noise
+ *                does not enter), Algorithm 1's hardened width;
+ *   bbar       = (1/n_groups) sum_g sum_k pi_{g,k} B_k (double), the expected
+ *                bit cost of section 3.2.
+ * Arguments (all device pointers, caller-owned; the call only enqueues work):
+ *   W_dev        float[n_groups*64] weights, 16-byte aligned.  Each group's
+ *                max|w| must be below 65520 (its 2-bit scale is an fp16 value);
+ *                a group outside that range or with NaN/Inf gives non-finite
+ *                outputs for that group (not checked).
+ *   logits_dev   float[n_groups][4], 16-byte aligned.
+ *   noise_dev    float[n_groups][4] Gumbel noise drawn by the caller, 16-byte
+ *                aligned, or NULL for no noise (plain softmax).
+ *   tau          temperature, finite and > 0.
+ *   w_soft_dev   float[n_groups*64] output, 16-byte aligned; may not overlap
+ *                the inputs.
+ *   pi_dev       float[n_groups][4] output (16-byte aligned) or NULL.
+ *   hard_bits_dev uint8[n_groups] output or NULL.
+ *   bbar_dev     one double output (8-byte aligned) or NULL; needs a workspace
+ *                of vbq_qat_workspace_size bytes (8-byte aligned), whose
+ *                contents are scratch.  bbar is summed in a fixed order, so
+ *                repeated calls give the same bits.
+ * n_groups == 0 does nothing (any pointer may then be NULL; bbar is not
+ * written).  Errors: VBQ_ERR_NULL (W, logits or w_soft NULL; workspace NULL
+ * with bbar), VBQ_ERR_SHAPE (n_groups out of range),
+ * VBQ_ERR_NONFINITE (tau NaN/Inf), VBQ_ERR_UNSUPPORTED (tau <= 0),
+ * VBQ_ERR_BUFFER (misaligned pointer or workspace too small), VBQ_ERR_HIP. */
+vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev,
+                           const float* logits_dev, const float* noise_dev,
+                           float tau, float* w_soft_dev, float* pi_dev,
+                           uint8_t* hard_bits_dev, double* bbar_dev,
+                           void* workspace_dev, size_t workspace_bytes,
+                           void* stream);
 
 #ifdef __cplusplus
 }

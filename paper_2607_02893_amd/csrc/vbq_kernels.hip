@@ -1644,6 +1644,10 @@ vbq_status launch_mm(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
 
 }  // namespace
 
+// Shared with the other device sources of the library: records a failed HIP
+// call for vbq_last_hip_error and maps it to a status.
+vbq_status vbq_detail_hip_status(hipError_t e) { return hip_status(e); }
+
 extern "C" {
 
 const char* vbq_last_hip_error(void) { return hipGetErrorName(g_last_hip_error); }

@@ -17,6 +17,14 @@ used):
     {-(2^(b-1)-1) .. 2^(b-1)-1} for b >= 2 and {-1, +1} for b = 1;
   * activations: N(0, 1) rounded to fp16, from key (layer, proj, 1000 + m).
 
+Selection path (paper section 3.2, training time): flat fp32 weights whose
+64-weight groups are N(0, sigma_g^2) with sigma_g log-uniform in
+[1e-3, 0.1] (groups of very different magnitude, as across a network's
+layers), logits N(0, 1.5^2) per (group, candidate) and standard Gumbel noise
+-log(-log U) per (group, candidate), drawn in that order from key
+(3000, part).  The training-step workload is the flat concatenation of the
+131M-class model's linear weights (workload 1's matrices, 137.8M weights).
+
 Recipe variant (paper section 4, the fixed recipe that is deployed): the
 first block's MLP (gate, up, down) at 4 bits, every other projection at
 2 bits, and the LM head tiered per row by token-frequency rank -- top 0.5% of
@@ -222,3 +230,29 @@ def make_matrix(spec, seed):
 
 def make_x(spec, seed, M=1):
     return draw_x(rng_for(seed, spec.layer, spec.proj, 1000), M, spec.K)
+
+
+# ---------------------------------------------------- differentiable bit selection
+
+SELECTION_SEED = 20260760
+
+
+def draw_selection_inputs(rng, n_groups, sigma_lo=1e-3, sigma_hi=0.1, logit_std=1.5):
+    """(W float32[n_groups*64], logits float32[n_groups, 4], noise float32[n_groups, 4])."""
+    sigma = np.exp(rng.uniform(np.log(sigma_lo), np.log(sigma_hi), size=n_groups)).astype(np.float32)
+    W = rng.standard_normal((n_groups, G), dtype=np.float32) * sigma[:, None]
+    logits = rng.standard_normal((n_groups, 4), dtype=np.float32) * np.float32(logit_std)
+    noise = rng.gumbel(size=(n_groups, 4)).astype(np.float32)
+    return W.reshape(-1), logits, noise
+
+
+def selection_inputs(n_groups, part=0, seed=SELECTION_SEED):
+    return draw_selection_inputs(rng_for(seed, 3000, part), n_groups)
+
+
+def selection_workload(cfg=1):
+    """(name, [(matrix name, N, K)], total groups) of a model's linear weights
+    laid end to end, the unit of one training step of the selection path."""
+    w = workload(cfg)
+    mats = [(f"{m.name}{m.layer}", m.N, m.K) for m in w.matrices]
+    return w.name, mats, sum(N * K // G for _, N, K in mats)

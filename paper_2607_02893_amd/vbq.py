@@ -55,7 +55,10 @@ STATUS = {0: "VBQ_OK", 1: "VBQ_ERR_NULL", 2: "VBQ_ERR_SHAPE", 3: "VBQ_ERR_BITS",
           9: "VBQ_ERR_HIP", 10: "VBQ_ERR_UNSUPPORTED"}
 # exported symbols, in the order include/vbq.h declares them
 EXPORTS = ("vbq_status_string", "vbq_last_hip_error", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
-           "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_gemm_small", "vbq_dequant")
+           "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_gemm_small", "vbq_dequant",
+           "vbq_qat_workspace_size", "vbq_qat_forward")
+QAT_MAX_GROUPS = 1 << 40
+QAT_CANDIDATES = (1, 2, 4, 8)
 
 
 class VbqDesc(ctypes.Structure):
@@ -108,6 +111,10 @@ _lib.vbq_gemm_small.argtypes = [ctypes.POINTER(VbqDesc), _P, ctypes.c_int64, _P,
                                 ctypes.c_int64, _P]
 _lib.vbq_dequant.restype = ctypes.c_int
 _lib.vbq_dequant.argtypes = [ctypes.POINTER(VbqDesc), _P, _P, _P]
+_lib.vbq_qat_workspace_size.restype = ctypes.c_int
+_lib.vbq_qat_workspace_size.argtypes = [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]
+_lib.vbq_qat_forward.restype = ctypes.c_int
+_lib.vbq_qat_forward.argtypes = [ctypes.c_int64, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
 
 
 class VbqError(RuntimeError):
@@ -309,6 +316,70 @@ class BucketedMatrix:
         for _, Wp, rows in self.parts:
             Wp.gemv_rows(x, y, rows, stream)
         return y
+
+
+# ------------------------------------------------- differentiable bit selection
+
+def qat_workspace_size(n_groups):
+    """Device workspace bytes vbq_qat_forward needs for bbar over n_groups groups."""
+    nbytes = ctypes.c_size_t(0)
+    _check(_lib.vbq_qat_workspace_size(int(n_groups), ctypes.byref(nbytes)), "vbq_qat_workspace_size")
+    return nbytes.value
+
+
+def _dev_ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def qat_forward(W, logits, noise, tau, w_soft=None, pi=True, hard_bits=True, bbar=True, workspace=None,
+                stream=None):
+    """Forward pass of the selection path (paper section 3.2, Algorithm 1) on device tensors.
+
+    W: contiguous float32 device tensor whose numel is a multiple of 64 (its
+    groups are consecutive runs of 64; a row-major [N, K] matrix with K % 64 == 0
+    qualifies).  logits / noise: contiguous float32 [n_groups, 4] (any shape of
+    that size); noise may be None.  pi / hard_bits / bbar: True to allocate the
+    output, a tensor to write into, or False/None to skip it.  Returns
+    (w_soft, pi, hard_bits, bbar) with bbar a float64 device tensor of one
+    element (None where skipped).
+    """
+    import torch
+    if W.dtype != torch.float32 or not W.is_contiguous() or W.numel() % 64:
+        raise ValueError("W must be a contiguous float32 tensor with a multiple of 64 elements")
+    n = W.numel() // 64
+    for name, t in (("logits", logits), ("noise", noise)):
+        if t is not None and (t.dtype != torch.float32 or not t.is_contiguous() or t.numel() != 4 * n):
+            raise ValueError(f"{name} must be a contiguous float32 tensor of n_groups*4 elements")
+    dev = W.device
+    if w_soft is None:
+        w_soft = torch.empty_like(W)
+    if pi is True:
+        pi = torch.empty((n, 4), dtype=torch.float32, device=dev)
+    if hard_bits is True:
+        hard_bits = torch.empty(n, dtype=torch.uint8, device=dev)
+    if bbar is True:
+        bbar = torch.empty(1, dtype=torch.float64, device=dev)
+    pi = pi if pi is not False else None
+    hard_bits = hard_bits if hard_bits is not False else None
+    bbar = bbar if bbar is not False else None
+    ws_bytes = 0
+    if bbar is not None:
+        ws_bytes = qat_workspace_size(n)
+        if workspace is None:
+            workspace = torch.empty(max(ws_bytes, 8), dtype=torch.uint8, device=dev)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(_lib.vbq_qat_forward(n, _dev_ptr(W), _dev_ptr(logits), _dev_ptr(noise), float(tau), _dev_ptr(w_soft),
+                                _dev_ptr(pi), _dev_ptr(hard_bits), _dev_ptr(bbar), _dev_ptr(workspace), ws_bytes,
+                                _stream_handle(stream)), "vbq_qat_forward")
+    return w_soft, pi, hard_bits, bbar
+
+
+def raw_qat_forward(n_groups, W_ptr, logits_ptr, noise_ptr, tau, w_soft_ptr, pi_ptr, hard_ptr, bbar_ptr,
+                    ws_ptr, ws_bytes, stream_ptr):
+    """vbq_qat_forward on raw device addresses (0 for NULL)."""
+    v = lambda p: ctypes.c_void_p(p) if p else None  # noqa: E731
+    return _lib.vbq_qat_forward(int(n_groups), v(W_ptr), v(logits_ptr), v(noise_ptr), float(tau), v(w_soft_ptr),
+                                v(pi_ptr), v(hard_ptr), v(bbar_ptr), v(ws_ptr), int(ws_bytes), v(stream_ptr))
 
 
 def raw_gemv(desc, blob_ptr, x_ptr, y_ptr, stream_ptr):

@@ -252,3 +252,47 @@ def test_pack_row_buckets_rejects_mixed_rows():
     bits, q, s = synth.make_matrix(spec, 73)  # per-group widths
     with pytest.raises(ValueError):
         vbq.pack_row_buckets(q, s, bits)
+
+
+# ------------------------------------------------- differentiable bit selection
+
+def test_qat_workspace_size():
+    assert vbq.qat_workspace_size(0) == 0
+    assert vbq.qat_workspace_size(1) == 8
+    assert vbq.qat_workspace_size(64) == 8
+    assert vbq.qat_workspace_size(65) == 16
+    big = vbq.qat_workspace_size(10 ** 9)
+    assert big % 8 == 0 and 8 <= big <= 64 * 1024  # bounded by the launch, not by the size
+    lib = vbq.lib()
+    nb = ctypes.c_size_t(0)
+    assert lib.vbq_qat_workspace_size(-1, ctypes.byref(nb)) == 2
+    assert lib.vbq_qat_workspace_size(vbq.QAT_MAX_GROUPS + 1, ctypes.byref(nb)) == 2
+    assert lib.vbq_qat_workspace_size(5, None) == 1
+
+
+def test_qat_forward_argument_errors():
+    # every case is rejected before anything is launched (fake, aligned addresses)
+    A = 1 << 20  # a 16-byte aligned stand-in address, never dereferenced
+    f = vbq.raw_qat_forward
+    assert f(0, A, A, 0, 1.0, A, 0, 0, 0, 0, 0, 0) == 0            # n_groups == 0: nothing to do
+    assert f(0, 0, 0, 0, 1.0, 0, 0, 0, A, 0, 0, 0) == 0            # ... and pointers may be NULL
+    assert f(0, A, A, 0, 0.0, A, 0, 0, 0, 0, 0, 0) == 10           # tau is checked first
+    assert f(4, 0, A, 0, 1.0, A, 0, 0, 0, 0, 0, 0) == 1            # W NULL
+    assert f(4, A, 0, 0, 1.0, A, 0, 0, 0, 0, 0, 0) == 1            # logits NULL
+    assert f(4, A, A, 0, 1.0, 0, 0, 0, 0, 0, 0, 0) == 1            # w_soft NULL
+    assert f(-1, A, A, 0, 1.0, A, 0, 0, 0, 0, 0, 0) == 2           # n_groups < 0
+    assert f(vbq.QAT_MAX_GROUPS + 1, A, A, 0, 1.0, A, 0, 0, 0, 0, 0, 0) == 2
+    assert f(4, A, A, 0, float("nan"), A, 0, 0, 0, 0, 0, 0) == 5   # tau NaN
+    assert f(4, A, A, 0, float("inf"), A, 0, 0, 0, 0, 0, 0) == 5   # tau Inf
+    assert f(4, A, A, 0, 0.0, A, 0, 0, 0, 0, 0, 0) == 10           # tau == 0
+    assert f(4, A, A, 0, -0.5, A, 0, 0, 0, 0, 0, 0) == 10          # tau < 0
+    assert f(4, A + 4, A, 0, 1.0, A, 0, 0, 0, 0, 0, 0) == 7        # W misaligned
+    assert f(4, A, A + 8, 0, 1.0, A, 0, 0, 0, 0, 0, 0) == 7        # logits misaligned
+    assert f(4, A, A, A + 4, 1.0, A, 0, 0, 0, 0, 0, 0) == 7        # noise misaligned
+    assert f(4, A, A, 0, 1.0, A + 4, 0, 0, 0, 0, 0, 0) == 7        # w_soft misaligned
+    assert f(4, A, A, 0, 1.0, A, A + 4, 0, 0, 0, 0, 0) == 7        # pi misaligned
+    assert f(4, A, A, 0, 1.0, A, 0, 0, A, 0, 0, 0) == 1            # bbar without workspace
+    assert f(4, A, A, 0, 1.0, A, 0, 0, A + 4, A, 8, 0) == 7        # bbar misaligned
+    assert f(4, A, A, 0, 1.0, A, 0, 0, A, A + 4, 8, 0) == 7        # workspace misaligned
+    assert f(100, A, A, 0, 1.0, A, 0, 0, A, A, 8, 0) == 7          # workspace too small (needs 16)
+    assert f(0, A, A, 0, 1.0, A, 0, 0, A, A, 0, 0) == 0            # empty: workspace of 0 bytes is enough
