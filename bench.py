@@ -8,6 +8,7 @@ resident in HBM before timing starts.  Default workload: the 9B-class step
 from the {1:.69, 2:.15, 4:.12, 8:.04} mix), 129 GEMVs, ~1.95 GB streamed.
 
     python bench.py [--steps K] [--warmup W] [--workload 0..4] [--gpus 1]
+    python bench.py --qat     # the selection-path forward (training), its own JSON line
 
 Prints one JSON line.  `value` is effective GB/s = algorithmic bytes of the
 step / wall time per step (HIP-graph replay of the step).  The roofline block
@@ -39,40 +40,53 @@ TRAFFIC_CONFIG = "workload 3, M 1, widths mixed"  # the only configuration the c
 CALIB_BYTES = 256 << 20  # plain copy used to scale the HBM byte counters
 
 
-def kernel_source_hash():
+# the selection-path forward (--qat): its own kernel source and counter summary
+QAT_SOURCES = [os.path.join(ROOT, "paper_2607_02893_amd", "csrc", "vbq_select.hip")]
+QAT_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "vbq_qat_forward_kernel_131m_step_traffic.md")
+QAT_TRAFFIC_CONFIG = "selection forward, 131M-class linear weights"
+QAT_METRIC = ("selection-path forward (four candidate reconstructions + Gumbel-Softmax mix per 64-weight group) "
+              "effective HBM GB/s and µs per training step")
+# bytes per group: W and w_soft (64 fp32 each), logits, noise and pi (4 fp32 each), hardened width (1 byte)
+QAT_BYTES_PER_GROUP = 256 + 256 + 16 + 16 + 16 + 1
+
+
+def kernel_source_hash(sources=None):
     import hashlib
     h = hashlib.sha256()
-    for path in KERNEL_SOURCES:
+    for path in (KERNEL_SOURCES if sources is None else sources):
         with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def measured_traffic(config):
-    """HBM bytes per GEMV launch from the committed counter summary, or None
-    when that summary is missing, was taken on another kernel source, or on
-    another configuration than `config`."""
-    if config != TRAFFIC_CONFIG:
+def measured_traffic(config, path=None, expected_config=None, sources=None):
+    """HBM bytes per launch from a committed counter summary, or None when that
+    summary is missing, was taken on another kernel source, or on another
+    configuration than `config`."""
+    path = TRAFFIC_FILE if path is None else path
+    expected_config = TRAFFIC_CONFIG if expected_config is None else expected_config
+    if config != expected_config:
         return None
     try:
         fields = {}
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             for line in f:
                 if ":" in line and line.startswith("- "):
                     k, v = line[2:].split(":", 1)
                     v = v.strip()
                     fields[k.strip()] = v.split("`")[1] if v.startswith("`") else v
-        if fields.get("kernel_source_sha256") != kernel_source_hash() or fields.get("config") != TRAFFIC_CONFIG:
+        if fields.get("kernel_source_sha256") != kernel_source_hash(sources) or fields.get("config") != expected_config:
             return None
         return int(fields["hbm_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
         return None
 
 
-def pmc_summary(fetch_dir, write_dir):
+def pmc_summary(fetch_dir, write_dir, kernel="vbq_mv_", sources=None):
     """Summarise two rocprofv3 --pmc runs of `bench.py --profile` (FETCH_SIZE,
-    then WRITE_SIZE): per-launch KiB of the GEMV kernels, scaled by what the
-    same counters read for the calibration copy of CALIB_BYTES."""
+    then WRITE_SIZE): per-launch KiB of the kernels whose name contains
+    `kernel`, scaled by what the same counters read for the calibration copy
+    of CALIB_BYTES."""
     import csv
     import glob
 
@@ -83,8 +97,8 @@ def pmc_summary(fetch_dir, write_dir):
             if r["Counter_Name"] != counter:
                 continue
             name = r["Kernel_Name"]
-            # every one-row GEMV kernel of the step (per-unit and two-waves-per-unit)
-            key = "vbq" if "vbq_mv_" in name else ("copy" if "MulFunctor" in name else None)
+            # e.g. every one-row GEMV kernel of the decode step (per-unit and two-waves-per-unit)
+            key = "vbq" if kernel in name else ("copy" if "MulFunctor" in name else None)
             if key is None:
                 continue
             acc.setdefault(key, {}).setdefault(r["Dispatch_Id"], 0.0)
@@ -102,7 +116,7 @@ def pmc_summary(fetch_dir, write_dir):
             "write_kib_per_launch_raw": float(np.mean(wv)), "copy_fetch_kib": f_copy, "copy_write_kib": w_copy,
             "fetch_scale": f_scale, "write_scale": w_scale, "fetch_bytes_per_launch": fetch_b,
             "write_bytes_per_launch": write_b, "hbm_bytes_per_launch": int(round(fetch_b + write_b)),
-            "kernel_source_sha256": kernel_source_hash()}
+            "kernel_source_sha256": kernel_source_hash(sources)}
 
 
 def log(msg):
@@ -228,6 +242,221 @@ def write_traffic_file(path, summ):
         f.write("\n".join(lines) + "\n")
 
 
+def write_qat_traffic_file(path, summ):
+    """Counter summary of the selection-path forward kernel (read back by measured_traffic)."""
+    lines = [
+        "# HBM traffic of vbq_qat_forward_kernel: 131M-class training step (one launch)",
+        "",
+        "Two counter passes over `bench.py --qat --profile --steps 2 --warmup 1` (3 forward launches over the",
+        "131M-class model's 137.8M linear weights), then a plain copy of 256 MiB (torch.mul by 1.0) to",
+        "scale the counters to bytes:",
+        "",
+        "```",
+        "cd /tmp && export TMPDIR=/tmp",
+        "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pmc_qat_fetch -o run -- "
+        "python3 $R/bench.py --qat --profile --steps 2 --warmup 1",
+        "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pmc_qat_write -o run -- "
+        "python3 $R/bench.py --qat --profile --steps 2 --warmup 1",
+        "python3 bench.py --qat --pmc-summary gpurun_out/pmc_qat_fetch gpurun_out/pmc_qat_write "
+        "--write-traffic <this file>",
+        "```",
+        "",
+        "(`$R` is the repository root.)  Per-launch figures, averaged over the forward launches:",
+        "",
+        f"- config: {QAT_TRAFFIC_CONFIG}",
+        f"- launches: {summ['launches']}",
+        f"- fetch_kib_per_launch_raw: {summ['fetch_kib_per_launch_raw']:.1f}",
+        f"- write_kib_per_launch_raw: {summ['write_kib_per_launch_raw']:.1f}",
+        f"- copy_fetch_kib (256 MiB read): {summ['copy_fetch_kib']:.0f}",
+        f"- copy_write_kib (256 MiB written): {summ['copy_write_kib']:.0f}",
+        f"- fetch_scale: {summ['fetch_scale']:.4f}",
+        f"- write_scale: {summ['write_scale']:.4f}",
+        f"- fetch_bytes_per_launch: {summ['fetch_bytes_per_launch']:.0f}",
+        f"- write_bytes_per_launch: {summ['write_bytes_per_launch']:.0f}",
+        f"- hbm_bytes_per_launch: {summ['hbm_bytes_per_launch']}",
+        f"- kernel_source_sha256: `{summ['kernel_source_sha256']}` (vbq_select.hip)",
+        "",
+        "bench.py --qat reports hbm_bytes_per_launch as roofline.traffic while the kernel source still has this hash.",
+    ]
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def qat_cpu_baseline(W, logits, noise, tau, n, budget_s=20.0):
+    """Oracle (numpy fp64) forward on consecutive chunks of groups until the
+    time budget is spent, scaled by group count to the whole step."""
+    from oracle import qat as oqat
+    chunk = 16384
+    done, spent = 0, 0.0
+    while done < n and spent < budget_s:
+        c = min(chunk, n - done)
+        w = W[64 * done:64 * (done + c)].reshape(c, 64)
+        t0 = time.perf_counter()
+        oqat.forward(w, logits[done:done + c].reshape(c, 1, 4), noise[done:done + c].reshape(c, 1, 4), tau)
+        spent += time.perf_counter() - t0
+        done += c
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = None
+    s_per_step = spent * n / done
+    cores = len(os.sched_getaffinity(0))
+    return {"value": round(1e3 * s_per_step, 1), "unit": "ms/step", "cores": threads or cores,
+            "host_cores_visible": cores, "kind": "oracle",
+            "sample": f"first {done} of {n} groups ({done * 64 / 1e6:.1f}M of {n * 64 / 1e6:.1f}M weights) in "
+                      f"chunks of {chunk}, {spent:.1f}s, scaled by group count"}
+
+
+def main_qat(args):
+    """--qat: the selection-path forward over the 131M-class model's linear
+    weights laid end to end (paper section 3.2, Algorithm 1), one launch of the
+    forward kernel plus the bbar reduction per step."""
+    from paper_2607_02893_amd import synth
+    name, mats, n = synth.selection_workload(1)
+    tau = 0.5
+    t0 = time.time()
+    W, logits, noise = synth.selection_inputs(n, part=1)
+    log(f"{name}: {len(mats)} matrices, {n} groups ({n * 64 / 1e6:.1f}M weights), inputs drawn in "
+        f"{time.time() - t0:.1f}s")
+
+    import torch
+    from paper_2607_02893_amd import vbq
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    Wd = torch.from_numpy(W).to(dev)
+    ld = torch.from_numpy(logits).to(dev)
+    nd = torch.from_numpy(noise).to(dev)
+    ws = torch.empty_like(Wd)
+    pi = torch.empty((n, 4), dtype=torch.float32, device=dev)
+    hard = torch.empty(n, dtype=torch.uint8, device=dev)
+    bbar = torch.empty(1, dtype=torch.float64, device=dev)
+    ws_bytes = vbq.qat_workspace_size(n)
+    work = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+    blocks = ws_bytes // 8
+    alg_kernel = n * QAT_BYTES_PER_GROUP + 8 * blocks          # the forward kernel (its partial sums included)
+    alg_step = alg_kernel + 8 * blocks + 8                      # + the bbar reduction
+
+    def fwd(with_bbar=True):
+        st = vbq.raw_qat_forward(n, Wd.data_ptr(), ld.data_ptr(), nd.data_ptr(), tau, ws.data_ptr(), pi.data_ptr(),
+                                 hard.data_ptr(), bbar.data_ptr() if with_bbar else 0,
+                                 work.data_ptr() if with_bbar else 0, ws_bytes if with_bbar else 0, sptr)
+        if st != 0:
+            raise vbq.VbqError(st, "vbq_qat_forward")
+
+    for _ in range(args.warmup):
+        fwd()
+    torch.cuda.synchronize()
+    if args.profile:
+        # the launches the roofline times (the forward kernel alone, back to back),
+        # then a few whole steps (forward + bbar)
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            fwd(False)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        for _ in range(3):
+            fwd()
+        torch.cuda.synchronize()
+        src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_run": True, "us_per_step_eager": round(1e6 * dt, 2)}), flush=True)
+        return
+
+    def timed(run, k):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(k):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / k, e0.elapsed_time(e1) * 1e-3 / k
+
+    wall_s, gpu_s = timed(fwd, args.steps)
+    log(f"step (forward + bbar): {1e6 * wall_s:.1f} us wall, {1e6 * gpu_s:.1f} us events")
+    # the forward kernel alone, K launches back to back on the same stream
+    _, kern_s = timed(lambda: fwd(False), args.steps)
+    log(f"forward kernel alone: {1e6 * kern_s:.1f} us per launch")
+    # the logit step's gradient (Algorithm 1, every m-th step): same weights, a
+    # seeded dL/dw_soft, the forward's pi
+    grad = torch.from_numpy(synth.rng_for(synth.SELECTION_SEED, 3004, 1).standard_normal(
+        n * 64, dtype=np.float32)).to(dev)
+    dlog = torch.empty((n, 4), dtype=torch.float32, device=dev)
+
+    def lgrad():
+        st = vbq.raw_qat_logit_grad(n, Wd.data_ptr(), grad.data_ptr(), pi.data_ptr(), tau, 0.05, n,
+                                    dlog.data_ptr(), sptr)
+        if st != 0:
+            raise vbq.VbqError(st, "vbq_qat_logit_grad")
+    for _ in range(3):
+        lgrad()
+    _, grad_s = timed(lgrad, args.steps)
+    alg_grad = n * (256 + 256 + 16 + 16)
+    log(f"logit-step gradient: {1e6 * grad_s:.1f} us per launch, {alg_grad / grad_s / 1e9:.0f} GB/s")
+    del grad
+    torch.cuda.synchronize()
+    value = alg_step / wall_s / 1e9
+    achieved = alg_kernel / kern_s / 1e9
+    traffic = measured_traffic(QAT_TRAFFIC_CONFIG, QAT_TRAFFIC_FILE, QAT_TRAFFIC_CONFIG, QAT_SOURCES)
+    # plain copy of the same bytes through torch (context: what the chip streams)
+    cp_src = torch.empty(n * 64 + n * 12, dtype=torch.float32, device=dev)
+    cp_dst = torch.empty_like(cp_src)
+    for _ in range(3):
+        cp_dst.copy_(cp_src)
+    _, copy_s = timed(lambda: cp_dst.copy_(cp_src), max(5, args.steps // 4))
+    copy_gbs = 2 * cp_src.numel() * 4 / copy_s / 1e9
+    log(f"torch copy of {2 * cp_src.numel() * 4 / 1e6:.0f} MB (read + write): {1e6 * copy_s:.1f} us, {copy_gbs:.0f} GB/s")
+    del cp_src, cp_dst
+    cpu = None
+    if not args.no_cpu:
+        cpu = qat_cpu_baseline(W, logits, noise, tau, n)
+        log(f"cpu oracle: {cpu['value']} ms/step ({cpu['sample']})")
+    out = {
+        "metric": QAT_METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * wall_s, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "precision": "fp32 weights in and out, fp16-rounded scales, double-precision group statistics",
+        "data": "synthetic (seeded draws; no trained weights)",
+        "config": {"workload": f"{name} selection-path forward: the linear weights of {len(mats)} matrices "
+                               f"end to end, {n * 64 / 1e6:.1f}M weights, {n} groups, tau {tau}",
+                   "algorithmic_bytes_per_step": int(alg_step)},
+        "us_per_step": round(1e6 * wall_s, 2),
+        "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+                     "kernel": "vbq_qat_forward_kernel",
+                     "launches_per_step": 1,
+                     "algorithmic_bytes_per_launch": int(alg_kernel),
+                     "avg_launch_us": round(1e6 * kern_s, 3),
+                     "timing": "HIP events on the launch stream around K launches of the kernel alone",
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "traffic_vs_algorithmic": round(traffic / alg_kernel, 3) if traffic else None},
+        "logit_grad": {"kernel": "vbq_qat_grad_kernel", "us_per_launch": round(1e6 * grad_s, 2),
+                       "algorithmic_bytes": int(alg_grad), "GBps": round(alg_grad / grad_s / 1e9, 1),
+                       "frac": round(alg_grad / grad_s / 1e9 / PEAK_HBM_GBS, 4),
+                       "note": "W and dL/dw_soft read, pi read, dL/dlogits written (Algorithm 1 logit step)"},
+        "copy_GBps": round(copy_gbs, 1),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -249,17 +478,24 @@ def main():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs of --profile (FETCH_SIZE, WRITE_SIZE) and exit")
     ap.add_argument("--write-traffic", metavar="PATH", help="with --pmc-summary: write the traffic summary file")
+    ap.add_argument("--qat", action="store_true",
+                    help="time the selection-path forward (training) over the 131M-class weights instead")
     args = ap.parse_args()
     if args.pmc_summary:
-        summ = pmc_summary(*args.pmc_summary)
+        if args.qat:
+            summ = pmc_summary(*args.pmc_summary, kernel="vbq_qat_forward_kernel", sources=QAT_SOURCES)
+        else:
+            summ = pmc_summary(*args.pmc_summary)
         print(json.dumps(summ), flush=True)
         if args.write_traffic:
-            write_traffic_file(args.write_traffic, summ)
+            (write_qat_traffic_file if args.qat else write_traffic_file)(args.write_traffic, summ)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the fused GEMV path has no multi-GPU mode in this build "
               "(the row / K split that would shard it is described in the design notes).", file=sys.stderr)
         sys.exit(2)
+    if args.qat:
+        return main_qat(args)
 
     if args.recipe and (args.batch != 1 or args.uniform):
         print("--recipe runs one activation row with the recipe's own widths", file=sys.stderr)

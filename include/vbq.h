@@ -266,6 +266,33 @@ vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev,
                            void* workspace_dev, size_t workspace_bytes,
                            void* stream);
 
+/* Gradient of the logit step (paper section 3.3, "Gradient isolation", and
+ * Algorithm 1): the candidate reconstructions are held constant, so with
+ * G = dL_CE/dw_soft the loss L = L_CE + lambda*bbar reaches the logits only
+ * through pi:
+ *   a_{g,k}     = sum_{i in g} G_i * w_hat^(B_k)_i + lambda * B_k / n_bbar
+ *   dlogits_g,k = (pi_{g,k} / tau) * (a_{g,k} - sum_j pi_{g,j} * a_{g,j}).
+ * The candidates are recomputed from W exactly as vbq_qat_forward forms them;
+ * the sums over a group are fp32 FMAs.
+ * Arguments (device pointers, caller-owned, 16-byte aligned; enqueued only):
+ *   W_dev        float[n_groups*64] the weights of the forward pass.
+ *   grad_dev     float[n_groups*64] dL_CE/dw_soft, same layout.
+ *   pi_dev       float[n_groups][4] the forward's pi (same tau and noise).
+ *   tau          the forward's temperature, finite and > 0.
+ *   lambda       the bit penalty, finite.
+ *   n_bbar       the n that divides bbar (>= 1): this array's n_groups for a
+ *                per-matrix penalty, the network's total group count when the
+ *                penalty is on the network's mean bits.
+ *   dlogits_dev  float[n_groups][4] output.
+ * n_groups == 0 does nothing (pointers may then be NULL).  Errors:
+ * VBQ_ERR_SHAPE (n_groups out of range, n_bbar < 1), VBQ_ERR_NONFINITE (tau
+ * or lambda NaN/Inf), VBQ_ERR_UNSUPPORTED (tau <= 0), VBQ_ERR_NULL,
+ * VBQ_ERR_BUFFER (misaligned), VBQ_ERR_HIP. */
+vbq_status vbq_qat_logit_grad(int64_t n_groups, const float* W_dev,
+                              const float* grad_dev, const float* pi_dev,
+                              float tau, float lambda, int64_t n_bbar,
+                              float* dlogits_dev, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

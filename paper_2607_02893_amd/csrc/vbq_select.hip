@@ -27,7 +27,9 @@
 //   * pi_{g,k} * s_k is folded once per group, so each weight costs one FMA
 //     per candidate in the mix;
 //   * the next slab's loads are issued before the current slab's arithmetic;
-//   * the results go back through LDS and out as coalesced 16-byte stores.
+//   * the results go back through LDS and out as coalesced 16-byte stores;
+//   * the bulk loads and stores carry the non-temporal hint, and the grid is
+//     2048 one-wave blocks (eight per CU), which measured fastest.
 
 #include <hip/hip_runtime.h>
 
@@ -44,8 +46,13 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kGroupsPerSlab = 64;  // one group per lane
 constexpr int kRowFloats = 68;      // LDS row of one group: 64 weights + 4 floats of padding
 constexpr int kMaxBlocks = 2048;    // one wave per block; eight resident blocks per CU on 256 CUs
+constexpr int kGradBlocks = 1024;   // the gradient's blocks hold two tiles: four resident per CU
 constexpr int kBbarThreads = 256;
 constexpr uint32_t kRsrcFlags = 0x00020000;
+// Cache policy of the bulk weight loads and w_soft stores: non-temporal (each
+// byte is touched once).  Measured on the 131M-class step: 221 us with the
+// hint, 253 us without; the hint on the small per-group arrays costs time.
+constexpr int kNonTemporal = 2;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, (int)kRsrcFlags);
@@ -93,6 +100,79 @@ __device__ __forceinline__ float exact_rne(float w, float q0, float s) {
   return step ? q0 + sg : q0;
 }
 
+// The four candidates' scales of one group (section 3.1), from the group's
+// 64 weights in the lane's LDS row: max|w| in fp32 (exact), the 1-bit absmean
+// as the sequential double sum / 64, every scale rounded once to fp16.
+struct Scales {
+  float s1;
+  Cand c2, c4, c8;
+};
+
+__device__ __forceinline__ Scales group_scales(uint32_t row_addr) {
+  float amax = 0.0f;
+  double asum = 0.0;
+#pragma unroll 4
+  for (int j = 0; j < 16; ++j) {
+    const u32x4 t = lds_u32x4(row_addr + 16u * j);
+    const float f[4] = {__uint_as_float(t.x), __uint_as_float(t.y), __uint_as_float(t.z), __uint_as_float(t.w)};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      amax = __builtin_fmaxf(amax, __builtin_fabsf(f[i]));
+      asum += (double)__builtin_fabsf(f[i]);  // sequential, weight 0 to 63
+    }
+  }
+  Scales sc;
+  sc.s1 = fp16_from_double(asum * (1.0 / 64.0));
+  sc.c2.s = fp16_from_double((double)amax);
+  sc.c4.s = fp16_from_double((double)amax / 7.0);
+  sc.c8.s = fp16_from_double((double)amax / 127.0);
+  sc.c2.qmax = 1.0f;
+  sc.c4.qmax = 7.0f;
+  sc.c8.qmax = 127.0f;
+  sc.c2.r = sc.c2.s > 0.0f ? __builtin_amdgcn_rcpf(sc.c2.s) : 0.0f;
+  sc.c4.r = sc.c4.s > 0.0f ? __builtin_amdgcn_rcpf(sc.c4.s) : 0.0f;
+  sc.c8.r = sc.c8.s > 0.0f ? __builtin_amdgcn_rcpf(sc.c8.s) : 0.0f;
+  return sc;
+}
+
+// Levels q = clip(round(x/s), -qmax, qmax) of the 2-, 4- and 8-bit candidates
+// (Eq. (1)), round-half-to-even exactly: rint(x * rcp(s)) is within 5e-5 of
+// x/s, so it is exact unless within 2^-12 of a half-integer; then the wave
+// takes the midpoint comparison for every lane.
+__device__ __forceinline__ void levels(float x, const Scales& sc, float& q2, float& q4, float& q8) {
+  constexpr float kNear = 0.5f - 1.0f / 4096.0f;
+  const float t2 = x * sc.c2.r, t4 = x * sc.c4.r, t8 = x * sc.c8.r;
+  q2 = __builtin_rintf(t2);
+  q4 = __builtin_rintf(t4);
+  q8 = __builtin_rintf(t8);
+  const bool near = __builtin_fabsf(t2 - q2) > kNear || __builtin_fabsf(t4 - q4) > kNear ||
+                    __builtin_fabsf(t8 - q8) > kNear;
+  if (__builtin_amdgcn_ballot_w64(near)) {
+    q2 = exact_rne(x, q2, sc.c2.s);
+    q4 = exact_rne(x, q4, sc.c4.s);
+    q8 = exact_rne(x, q8, sc.c8.s);
+  }
+  q2 = __builtin_amdgcn_fmed3f(q2, -sc.c2.qmax, sc.c2.qmax);
+  q4 = __builtin_amdgcn_fmed3f(q4, -sc.c4.qmax, sc.c4.qmax);
+  q8 = __builtin_amdgcn_fmed3f(q8, -sc.c8.qmax, sc.c8.qmax);
+}
+
+// LDS byte addresses of one lane: in the coalesced phase load j covers groups
+// 4j .. 4j+3 and lane l holds the 4 floats at (group 4j + l/16, weight
+// 4*(l%16)); in the lane-per-group phase lane l owns row l.
+struct TileAddr {
+  uint32_t co[16];
+  uint32_t row;
+};
+
+__device__ __forceinline__ TileAddr tile_addr(uint32_t base, uint32_t lane) {
+  TileAddr t;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) t.co[j] = base + 4u * ((4u * j + (lane >> 4)) * kRowFloats + 4u * (lane & 15u));
+  t.row = base + 4u * lane * kRowFloats;
+  return t;
+}
+
 struct QatArgs {
   const float* W;
   const float* logits;
@@ -110,12 +190,9 @@ __global__ __launch_bounds__(64) void vbq_qat_forward_kernel(QatArgs a) {
   __shared__ __attribute__((aligned(16))) float tile[kGroupsPerSlab * kRowFloats];
   const uint32_t lane = threadIdx.x;
   const uint32_t base = (uint32_t)(size_t)(__attribute__((address_space(3))) float*)tile;
-  // coalesced phase: load j covers groups 4j .. 4j+3, lane l the 4 floats at
-  // (4j + l/16, 4*(l%16)); the lane-per-group phase reads row `lane`
-  uint32_t co_addr[16];
-#pragma unroll
-  for (int j = 0; j < 16; ++j) co_addr[j] = base + 4u * ((4u * j + (lane >> 4)) * kRowFloats + 4u * (lane & 15u));
-  const uint32_t row_addr = base + 4u * lane * kRowFloats;
+  const TileAddr ta = tile_addr(base, lane);
+  const uint32_t* co_addr = ta.co;
+  const uint32_t row_addr = ta.row;
 
   double eb_sum = 0.0;
   int64_t slab = blockIdx.x;
@@ -128,7 +205,7 @@ __global__ __launch_bounds__(64) void vbq_qat_forward_kernel(QatArgs a) {
     const uint32_t ng = (uint32_t)(left < kGroupsPerSlab ? left : kGroupsPerSlab);
     const __amdgpu_buffer_rsrc_t rw = rsrc(a.W + g0 * 64, ng * 256u);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) v[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(j * 1024 + lane * 16), 0, 0);
+    for (int j = 0; j < 16; ++j) v[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
     lg = __builtin_amdgcn_raw_buffer_load_b128(rsrc(a.logits + g0 * 4, ng * 16u), (int)(lane * 16), 0, 0);
     if (a.noise) ns = __builtin_amdgcn_raw_buffer_load_b128(rsrc(a.noise + g0 * 4, ng * 16u), (int)(lane * 16), 0, 0);
   };
@@ -151,30 +228,9 @@ __global__ __launch_bounds__(64) void vbq_qat_forward_kernel(QatArgs a) {
     if (slab + stride < a.n_slabs) load_slab(slab + stride);
 
     // ---- group statistics and scales (section 3.1), streaming the lane's row
-    float amax = 0.0f;
-    double asum = 0.0;
-#pragma unroll 4
-    for (int j = 0; j < 16; ++j) {
-      const u32x4 t = lds_u32x4(row_addr + 16u * j);
-      const float f[4] = {__uint_as_float(t.x), __uint_as_float(t.y),
-                          __uint_as_float(t.z), __uint_as_float(t.w)};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        amax = __builtin_fmaxf(amax, __builtin_fabsf(f[i]));
-        asum += (double)__builtin_fabsf(f[i]);  // sequential, weight 0 to 63
-      }
-    }
-    const float s1 = fp16_from_double(asum * (1.0 / 64.0));
-    Cand c2, c4, c8;
-    c2.s = fp16_from_double((double)amax);
-    c4.s = fp16_from_double((double)amax / 7.0);
-    c8.s = fp16_from_double((double)amax / 127.0);
-    c2.qmax = 1.0f;
-    c4.qmax = 7.0f;
-    c8.qmax = 127.0f;
-    c2.r = c2.s > 0.0f ? __builtin_amdgcn_rcpf(c2.s) : 0.0f;
-    c4.r = c4.s > 0.0f ? __builtin_amdgcn_rcpf(c4.s) : 0.0f;
-    c8.r = c8.s > 0.0f ? __builtin_amdgcn_rcpf(c8.s) : 0.0f;
+    const Scales sc = group_scales(row_addr);
+    const float s1 = sc.s1;
+    Cand c2 = sc.c2, c4 = sc.c4, c8 = sc.c8;
 
     // ---- Gumbel-Softmax weights (section 3.2)
     const float z0 = (l0 + e0) / a.tau, z1 = (l1 + e1) / a.tau, z2 = (l2 + e2) / a.tau, z3 = (l3 + e3) / a.tau;
@@ -204,35 +260,22 @@ __global__ __launch_bounds__(64) void vbq_qat_forward_kernel(QatArgs a) {
     }
 
     // ---- the mix, four weights at a time, in place in the lane's row
-    constexpr float kNear = 0.5f - 1.0f / 4096.0f;
 #pragma unroll 2
     for (int j = 0; j < 16; ++j) {
       const u32x4 t = lds_u32x4(row_addr + 16u * j);
-      float f[4] = {__uint_as_float(t.x), __uint_as_float(t.y),
-                    __uint_as_float(t.z), __uint_as_float(t.w)};
+      float f[4] = {__uint_as_float(t.x), __uint_as_float(t.y), __uint_as_float(t.z), __uint_as_float(t.w)};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float x = f[i];
-        const float t2 = x * c2.r, t4 = x * c4.r, t8 = x * c8.r;
-        float q2 = __builtin_rintf(t2), q4 = __builtin_rintf(t4), q8 = __builtin_rintf(t8);
-        const bool near = __builtin_fabsf(t2 - q2) > kNear || __builtin_fabsf(t4 - q4) > kNear ||
-                          __builtin_fabsf(t8 - q8) > kNear;
-        if (__builtin_amdgcn_ballot_w64(near)) {
-          q2 = exact_rne(x, q2, c2.s);
-          q4 = exact_rne(x, q4, c4.s);
-          q8 = exact_rne(x, q8, c8.s);
-        }
-        q2 = __builtin_amdgcn_fmed3f(q2, -c2.qmax, c2.qmax);
-        q4 = __builtin_amdgcn_fmed3f(q4, -c4.qmax, c4.qmax);
-        q8 = __builtin_amdgcn_fmed3f(q8, -c8.qmax, c8.qmax);
+        float q2, q4, q8;
+        levels(x, sc, q2, q4, q8);
         float acc = x >= 0.0f ? c1 : -c1;  // sign(0) = +1 (also for -0.0)
         acc = __builtin_fmaf(c2.c, q2, acc);
         acc = __builtin_fmaf(c4.c, q4, acc);
         acc = __builtin_fmaf(c8.c, q8, acc);
         f[i] = acc;
       }
-      const u32x4 o = {__float_as_uint(f[0]), __float_as_uint(f[1]),
-                       __float_as_uint(f[2]), __float_as_uint(f[3])};
+      const u32x4 o = {__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]), __float_as_uint(f[3])};
       lds_store_u32x4(row_addr + 16u * j, o);
     }
 
@@ -240,7 +283,7 @@ __global__ __launch_bounds__(64) void vbq_qat_forward_kernel(QatArgs a) {
     __syncthreads();
     const __amdgpu_buffer_rsrc_t ro = rsrc(a.w_soft + g0 * 64, ng * 256u);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) __builtin_amdgcn_raw_buffer_store_b128(lds_u32x4(co_addr[j]), ro, (int)(j * 1024 + lane * 16), 0, 0);
+    for (int j = 0; j < 16; ++j) __builtin_amdgcn_raw_buffer_store_b128(lds_u32x4(co_addr[j]), ro, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
     __syncthreads();  // the next slab overwrites the tile
   }
 
@@ -249,6 +292,95 @@ __global__ __launch_bounds__(64) void vbq_qat_forward_kernel(QatArgs a) {
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) eb_sum += __shfl_xor(eb_sum, d, 64);
     if (lane == 0) a.partial[blockIdx.x] = eb_sum;
+  }
+}
+
+struct GradArgs {
+  const float* W;
+  const float* grad;   // dL/dw_soft
+  const float* pi;
+  float* dlogits;
+  float tau;
+  float lambda;
+  double n_bbar;       // the n of bbar
+  int64_t n_groups;
+  int64_t n_slabs;
+};
+
+// Logit step of Algorithm 1 (section 3.3): with the candidates held constant,
+//   a_k = sum_i G_i w_hat^(B_k)_i + lambda B_k / n,
+//   dL/dl_k = (pi_k / tau) (a_k - sum_j pi_j a_j).
+// Same slab walk as the forward, with the gradients transposed through a
+// second LDS tile next to the weights (both slabs loaded coalesced and
+// prefetched a slab ahead); 34 KiB of LDS per wave leaves four resident
+// blocks per CU, so the grid is kGradBlocks.  sum_i G_i w_hat^(b)_i =
+// s_b sum_i G_i q_i, so each weight costs four FMAs.
+__global__ __launch_bounds__(64) void vbq_qat_grad_kernel(GradArgs a) {
+  __shared__ __attribute__((aligned(16))) float tile[2 * kGroupsPerSlab * kRowFloats];
+  const uint32_t lane = threadIdx.x;
+  const uint32_t base = (uint32_t)(size_t)(__attribute__((address_space(3))) float*)tile;
+  const TileAddr tw = tile_addr(base, lane);
+  const TileAddr tg = tile_addr(base + 4u * kGroupsPerSlab * kRowFloats, lane);
+  const float pen1 = (float)((double)a.lambda * 1.0 / a.n_bbar), pen2 = (float)((double)a.lambda * 2.0 / a.n_bbar);
+  const float pen4 = (float)((double)a.lambda * 4.0 / a.n_bbar), pen8 = (float)((double)a.lambda * 8.0 / a.n_bbar);
+
+  int64_t slab = blockIdx.x;
+  const int64_t stride = gridDim.x;
+  u32x4 v[16], gv[16];
+  auto load_slab = [&](int64_t sl) {
+    const int64_t g0 = sl * kGroupsPerSlab;
+    const int64_t left = a.n_groups - g0;
+    const uint32_t ng = (uint32_t)(left < kGroupsPerSlab ? left : kGroupsPerSlab);
+    const __amdgpu_buffer_rsrc_t rw = rsrc(a.W + g0 * 64, ng * 256u);
+    const __amdgpu_buffer_rsrc_t rg = rsrc(a.grad + g0 * 64, ng * 256u);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      v[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
+      gv[j] = __builtin_amdgcn_raw_buffer_load_b128(rg, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
+    }
+  };
+  if (slab < a.n_slabs) load_slab(slab);
+
+  for (; slab < a.n_slabs; slab += stride) {
+    const int64_t g0 = slab * kGroupsPerSlab;
+    const int64_t left = a.n_groups - g0;
+    const uint32_t ng = (uint32_t)(left < kGroupsPerSlab ? left : kGroupsPerSlab);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      lds_store_u32x4(tw.co[j], v[j]);
+      lds_store_u32x4(tg.co[j], gv[j]);
+    }
+    __syncthreads();
+    const u32x4 pv = __builtin_amdgcn_raw_buffer_load_b128(rsrc(a.pi + g0 * 4, ng * 16u), (int)(lane * 16), 0, 0);
+    if (slab + stride < a.n_slabs) load_slab(slab + stride);
+
+    const Scales sc = group_scales(tw.row);
+    float d1 = 0.0f, d2 = 0.0f, d4 = 0.0f, d8 = 0.0f;  // sum_i G_i q_i per candidate
+#pragma unroll 2
+    for (int j = 0; j < 16; ++j) {
+      const u32x4 t = lds_u32x4(tw.row + 16u * j);
+      const u32x4 u = lds_u32x4(tg.row + 16u * j);
+      const float f[4] = {__uint_as_float(t.x), __uint_as_float(t.y), __uint_as_float(t.z), __uint_as_float(t.w)};
+      const float gr[4] = {__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w)};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float q2, q4, q8;
+        levels(f[i], sc, q2, q4, q8);
+        d1 += f[i] >= 0.0f ? gr[i] : -gr[i];  // sign(0) = +1
+        d2 = __builtin_fmaf(gr[i], q2, d2);
+        d4 = __builtin_fmaf(gr[i], q4, d4);
+        d8 = __builtin_fmaf(gr[i], q8, d8);
+      }
+    }
+    const float a1 = __builtin_fmaf(sc.s1, d1, pen1), a2 = __builtin_fmaf(sc.c2.s, d2, pen2);
+    const float a4 = __builtin_fmaf(sc.c4.s, d4, pen4), a8 = __builtin_fmaf(sc.c8.s, d8, pen8);
+    const float p0 = __uint_as_float(pv.x), p1 = __uint_as_float(pv.y), p2 = __uint_as_float(pv.z),
+                p3 = __uint_as_float(pv.w);
+    const float mean = (p0 * a1 + p1 * a2) + (p2 * a4 + p3 * a8);
+    const u32x4 out = {__float_as_uint(p0 / a.tau * (a1 - mean)), __float_as_uint(p1 / a.tau * (a2 - mean)),
+                       __float_as_uint(p2 / a.tau * (a4 - mean)), __float_as_uint(p3 / a.tau * (a8 - mean))};
+    __builtin_amdgcn_raw_buffer_store_b128(out, rsrc(a.dlogits + g0 * 4, ng * 16u), (int)(lane * 16), 0, 0);
+    __syncthreads();  // the next slab overwrites the tiles
   }
 }
 
@@ -324,6 +456,33 @@ vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev, const float* lo
   void* args2[] = {&part, &n, &ngd, &bbar_dev};
   return vbq_detail_hip_status(
       hipLaunchKernel((const void*)vbq_qat_bbar_kernel, dim3(1), dim3(kBbarThreads), args2, 0, s));
+}
+
+vbq_status vbq_qat_logit_grad(int64_t n_groups, const float* W_dev, const float* grad_dev, const float* pi_dev,
+                              float tau, float lambda, int64_t n_bbar, float* dlogits_dev, void* stream) {
+  if (n_groups < 0 || n_groups > VBQ_QAT_MAX_GROUPS) return VBQ_ERR_SHAPE;
+  if (!(tau == tau) || tau == __builtin_inff() || tau == -__builtin_inff()) return VBQ_ERR_NONFINITE;
+  if (!(lambda == lambda) || lambda == __builtin_inff() || lambda == -__builtin_inff()) return VBQ_ERR_NONFINITE;
+  if (!(tau > 0.0f)) return VBQ_ERR_UNSUPPORTED;
+  if (n_bbar < 1) return VBQ_ERR_SHAPE;
+  if (n_groups == 0) return VBQ_OK;
+  if (!W_dev || !grad_dev || !pi_dev || !dlogits_dev) return VBQ_ERR_NULL;
+  if (!aligned(W_dev, 16) || !aligned(grad_dev, 16) || !aligned(pi_dev, 16) || !aligned(dlogits_dev, 16))
+    return VBQ_ERR_BUFFER;
+  GradArgs a;
+  a.W = W_dev;
+  a.grad = grad_dev;
+  a.pi = pi_dev;
+  a.dlogits = dlogits_dev;
+  a.tau = tau;
+  a.lambda = lambda;
+  a.n_bbar = (double)n_bbar;
+  a.n_groups = n_groups;
+  a.n_slabs = (n_groups + kGroupsPerSlab - 1) / kGroupsPerSlab;
+  void* args[] = {&a};
+  const int64_t blocks = a.n_slabs < kGradBlocks ? a.n_slabs : kGradBlocks;
+  return vbq_detail_hip_status(hipLaunchKernel((const void*)vbq_qat_grad_kernel, dim3((unsigned)blocks), dim3(64),
+                                               args, 0, (hipStream_t)stream));
 }
 
 }  // extern "C"

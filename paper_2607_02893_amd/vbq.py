@@ -56,7 +56,7 @@ STATUS = {0: "VBQ_OK", 1: "VBQ_ERR_NULL", 2: "VBQ_ERR_SHAPE", 3: "VBQ_ERR_BITS",
 # exported symbols, in the order include/vbq.h declares them
 EXPORTS = ("vbq_status_string", "vbq_last_hip_error", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
            "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_gemm_small", "vbq_dequant",
-           "vbq_qat_workspace_size", "vbq_qat_forward")
+           "vbq_qat_workspace_size", "vbq_qat_forward", "vbq_qat_logit_grad")
 QAT_MAX_GROUPS = 1 << 40
 QAT_CANDIDATES = (1, 2, 4, 8)
 
@@ -115,6 +115,8 @@ _lib.vbq_qat_workspace_size.restype = ctypes.c_int
 _lib.vbq_qat_workspace_size.argtypes = [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]
 _lib.vbq_qat_forward.restype = ctypes.c_int
 _lib.vbq_qat_forward.argtypes = [ctypes.c_int64, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.vbq_qat_logit_grad.restype = ctypes.c_int
+_lib.vbq_qat_logit_grad.argtypes = [ctypes.c_int64, _P, _P, _P, ctypes.c_float, ctypes.c_float, ctypes.c_int64, _P, _P]
 
 
 class VbqError(RuntimeError):
@@ -372,6 +374,36 @@ def qat_forward(W, logits, noise, tau, w_soft=None, pi=True, hard_bits=True, bba
                                 _dev_ptr(pi), _dev_ptr(hard_bits), _dev_ptr(bbar), _dev_ptr(workspace), ws_bytes,
                                 _stream_handle(stream)), "vbq_qat_forward")
     return w_soft, pi, hard_bits, bbar
+
+
+def qat_logit_grad(W, grad, pi, tau, lam, n_bbar=None, dlogits=None, stream=None):
+    """Logit-step gradient (paper section 3.3, Algorithm 1) on device tensors.
+
+    W, grad: contiguous float32 tensors of n_groups*64 elements (the forward's
+    weights and dL_CE/dw_soft); pi: the forward's float32 [n_groups, 4];
+    n_bbar: the n of bbar (default n_groups).  Returns dL/dlogits, float32
+    [n_groups, 4].
+    """
+    import torch
+    for name, t, k in (("W", W, 64), ("grad", grad, 64), ("pi", pi, 4)):
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 tensor")
+    n = W.numel() // 64
+    if W.numel() % 64 or grad.numel() != W.numel() or pi.numel() != 4 * n:
+        raise ValueError("W and grad need n_groups*64 elements and pi n_groups*4")
+    if dlogits is None:
+        dlogits = torch.empty((n, 4), dtype=torch.float32, device=W.device)
+    _check(_lib.vbq_qat_logit_grad(n, _dev_ptr(W), _dev_ptr(grad), _dev_ptr(pi), float(tau), float(lam),
+                                   int(n if n_bbar is None else n_bbar), _dev_ptr(dlogits), _stream_handle(stream)),
+           "vbq_qat_logit_grad")
+    return dlogits
+
+
+def raw_qat_logit_grad(n_groups, W_ptr, grad_ptr, pi_ptr, tau, lam, n_bbar, d_ptr, stream_ptr):
+    """vbq_qat_logit_grad on raw device addresses (0 for NULL)."""
+    v = lambda p: ctypes.c_void_p(p) if p else None  # noqa: E731
+    return _lib.vbq_qat_logit_grad(int(n_groups), v(W_ptr), v(grad_ptr), v(pi_ptr), float(tau), float(lam),
+                                   int(n_bbar), v(d_ptr), v(stream_ptr))
 
 
 def raw_qat_forward(n_groups, W_ptr, logits_ptr, noise_ptr, tau, w_soft_ptr, pi_ptr, hard_ptr, bbar_ptr,

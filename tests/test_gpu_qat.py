@@ -1,4 +1,4 @@
-"""GPU parity of the selection path (vbq_qat_forward) against the oracle.
+"""GPU parity of the selection path (vbq_qat_forward, vbq_qat_logit_grad) against the oracle.
 
 Bars:
   * candidate reconstructions: exact.  A one-hot pi (logit margins so wide
@@ -6,7 +6,8 @@ Bars:
     equal the oracle's w_hat^(b) value for value, and equal vbq_dequant of
     vbq_pack at the hardened widths;
   * hardened widths: exact (argmax of the same fp32 logits on both sides);
-  * pi, w_soft, bbar: the fp32 arithmetic bound below.
+  * pi, w_soft, bbar: the fp32 arithmetic bound below;
+  * dL/dlogits of the logit step: the bound derived at _check_grad.
 
 Tolerance (derived from the fp32 arithmetic, u = 2^-24).  With
 z_k = (l_k + e_k)/tau and Z = max_k |z_k| for the group: the sum and the
@@ -259,3 +260,90 @@ def test_training_step_full_size(vbq):
     Wg = W.reshape(n, 64)[idx]
     _check_mix(Wg.reshape(-1), logits[idx], noise[idx], tau, w_soft.reshape(n, 64)[idx], pi[idx], None,
                "full size sampled")
+
+
+# ------------------------------------------------------------------ logit step
+
+def _grad_inputs(n, part, tau):
+    """Weights, dL/dw_soft and pi for the logit step.  pi is the oracle's softmax
+    of the seeded logits and noise, rounded to float32 (no input comes from the
+    kernels)."""
+    W, logits, noise = synth.selection_inputs(n, part=part)
+    G = synth.rng_for(synth.SELECTION_SEED, 3004, part).standard_normal(n * 64, dtype=np.float32)
+    pi = oqat.gumbel_softmax(logits, noise, tau).astype(np.float32)
+    return W, G, pi
+
+
+def _check_grad(W, G, pi, tau, lam, n_bbar, got, what):
+    """Bound (fp32, u = 2^-24): each a_k is a 64-term FMA sum scaled once and
+    offset once, within 67u (sum_i |G_i w_hat_k,i| + |lambda| B_k / n); the
+    pi-weighted mean, the difference and the scaling by pi_k / tau add a few u
+    of the same magnitudes.  Allowed: (pi_k / tau) * 96u * (A_k + sum_j pi_j A_j)."""
+    n = pi.shape[0]
+    Wg = W.reshape(n, 64).astype(np.float64)
+    want = oqat.logit_grad(Wg, G.reshape(n, 64), pi.reshape(n, 1, 4), tau, lam, n_groups=n_bbar).reshape(n, 4)
+    cand = oqat.candidates(Wg).reshape(4, n, 64)
+    A = np.einsum("gi,kgi->gk", np.abs(G.reshape(n, 64).astype(np.float64)), np.abs(cand)) + abs(lam) * WIDTHS / n_bbar
+    p = pi.astype(np.float64)
+    bound = p / tau * 96 * U * (A + np.sum(p * A, axis=-1, keepdims=True)) + 1e-37
+    err = np.abs(got.reshape(n, 4).astype(np.float64) - want)
+    bad = err > bound
+    assert not bad.any(), f"{what}: dlogits off at groups {np.nonzero(bad.any(axis=1))[0][:8]}"
+
+
+@pytest.mark.parametrize("lam", [0.0, 2.5])
+@pytest.mark.parametrize("tau", [5.0, 0.5])
+@pytest.mark.parametrize("n", [1, 65, 4097, 2 * 64 * 2048 + 77])
+def test_logit_grad_matches_oracle(vbq, n, tau, lam):
+    _say(f"qat logit grad n_groups={n} tau={tau} lambda={lam}")
+    W, G, pi = _grad_inputs(n, 50_000 + n, tau)
+    d = vbq.qat_logit_grad(_dev(W), _dev(G), _dev(pi), tau, lam)
+    torch.cuda.synchronize()
+    _check_grad(W, G, pi, tau, lam, n, d.cpu().numpy(), f"n={n} tau={tau} lambda={lam}")
+
+
+def test_logit_grad_golden(vbq, golden_dir):
+    import json
+    import os
+    with open(os.path.join(golden_dir, "qat_group.json")) as f:
+        g = json.load(f)
+    W = np.zeros(64, dtype=np.float32)
+    W[: len(g["w_head"])] = g["w_head"]
+    G = np.zeros(64, dtype=np.float32)
+    G[0] = g["logit_grad"]["grad_entry0"]
+    pi = np.asarray(g["mix"]["pi"], dtype=np.float32).reshape(1, 4)
+    d = vbq.qat_logit_grad(_dev(W), _dev(G), _dev(pi), g["mix"]["tau"], g["logit_grad"]["lambda"]).cpu().numpy()
+    # pi = (0.1, 0.2, 0.3, 0.4) rounded to float32: agreement to about 1e-7
+    np.testing.assert_allclose(d[0], g["logit_grad"]["dlogits"], rtol=1e-6, atol=1e-7)
+
+
+def test_logit_grad_rows_sum_to_zero_and_network_n(vbq):
+    # softmax gradient: each group's dlogits sum to 0; n_bbar only scales the penalty
+    n = 3000
+    W, G, pi = _grad_inputs(n, 60_000, 1.0)
+    d_local = vbq.qat_logit_grad(_dev(W), _dev(G), _dev(pi), 1.0, 3.0).cpu().numpy()
+    d_net = vbq.qat_logit_grad(_dev(W), _dev(G), _dev(pi), 1.0, 3.0, n_bbar=10 * n).cpu().numpy()
+    _check_grad(W, G, pi, 1.0, 3.0, 10 * n, d_net, "network n")
+    # sum_k dlogits_k = (1/tau)(sum_k pi_k a_k - mean * sum_k pi_k): zero up to the
+    # rounding of the a_k, which scales with their magnitudes A_k (not with |dlogits|)
+    Wg = W.reshape(n, 64).astype(np.float64)
+    cand = oqat.candidates(Wg).reshape(4, n, 64)
+    A = np.einsum("gi,kgi->gk", np.abs(G.reshape(n, 64).astype(np.float64)), np.abs(cand)) + 3.0 * WIDTHS / n
+    p = pi.astype(np.float64)
+    assert np.all(np.abs(d_local.astype(np.float64).sum(axis=1)) <= 2 * 96 * U * np.sum(p * A, axis=1) + 1e-37)
+    assert not np.array_equal(d_local, d_net)
+
+
+def test_logit_grad_full_size(vbq):
+    name, mats, n = synth.selection_workload(1)
+    _say(f"qat logit grad full size: {name} {n} groups")
+    tau, lam = 0.5, 0.05
+    W, G, pi = _grad_inputs(n, 2, tau)
+    d = vbq.qat_logit_grad(_dev(W), _dev(G), _dev(pi), tau, lam).cpu().numpy()
+    rng = synth.rng_for(synth.SELECTION_SEED, 3005)
+    bounds = np.cumsum([0] + [N * K // 64 for _, N, K in mats])
+    idx = np.unique(np.concatenate([[0, n - 1], bounds[:-1], bounds[1:] - 1, rng.integers(0, n, size=4000)]))
+    Wg = W.reshape(n, 64)[idx].reshape(-1)
+    Gg = G.reshape(n, 64)[idx].reshape(-1)
+    _check_grad(Wg, Gg, pi[idx], tau, lam, n, d[idx], "full size sampled")
+    assert np.all(np.isfinite(d))

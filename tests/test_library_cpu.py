@@ -296,3 +296,21 @@ def test_qat_forward_argument_errors():
     assert f(4, A, A, 0, 1.0, A, 0, 0, A, A + 4, 8, 0) == 7        # workspace misaligned
     assert f(100, A, A, 0, 1.0, A, 0, 0, A, A, 8, 0) == 7          # workspace too small (needs 16)
     assert f(0, A, A, 0, 1.0, A, 0, 0, A, A, 0, 0) == 0            # empty: workspace of 0 bytes is enough
+
+
+def test_qat_logit_grad_argument_errors():
+    A = 1 << 20
+    f = vbq.raw_qat_logit_grad
+    assert f(0, 0, 0, 0, 1.0, 0.5, 1, 0, 0) == 0                   # nothing to do
+    assert f(-1, A, A, A, 1.0, 0.5, 1, A, 0) == 2                  # n_groups < 0
+    assert f(4, A, A, A, 1.0, 0.5, 0, A, 0) == 2                   # n_bbar < 1
+    assert f(4, A, A, A, float("nan"), 0.5, 4, A, 0) == 5          # tau NaN
+    assert f(4, A, A, A, 1.0, float("inf"), 4, A, 0) == 5          # lambda Inf
+    assert f(4, A, A, A, -1.0, 0.5, 4, A, 0) == 10                 # tau < 0
+    assert f(4, 0, A, A, 1.0, 0.5, 4, A, 0) == 1                   # W NULL
+    assert f(4, A, 0, A, 1.0, 0.5, 4, A, 0) == 1                   # grad NULL
+    assert f(4, A, A, 0, 1.0, 0.5, 4, A, 0) == 1                   # pi NULL
+    assert f(4, A, A, A, 1.0, 0.5, 4, 0, 0) == 1                   # dlogits NULL
+    assert f(4, A + 4, A, A, 1.0, 0.5, 4, A, 0) == 7               # misaligned
+    assert f(4, A, A, A + 8, 1.0, 0.5, 4, A, 0) == 7
+    assert f(4, A, A, A, 1.0, 0.5, 4, A + 4, 0) == 7
