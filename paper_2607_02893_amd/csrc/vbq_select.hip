@@ -46,7 +46,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kGroupsPerSlab = 64;  // one group per lane
 constexpr int kRowFloats = 68;      // LDS row of one group: 64 weights + 4 floats of padding
 constexpr int kMaxBlocks = 2048;    // one wave per block; eight resident blocks per CU on 256 CUs
-constexpr int kGradBlocks = 1024;   // the gradient's blocks hold two tiles: four resident per CU
+constexpr int kGradBlocks = 2048;   // the gradient's blocks: one tile + a 2 KiB table, eight resident per CU
 constexpr int kBbarThreads = 256;
 constexpr uint32_t kRsrcFlags = 0x00020000;
 // Cache policy of the bulk weight loads and w_soft stores: non-temporal (each
@@ -307,61 +307,104 @@ struct GradArgs {
   int64_t n_slabs;
 };
 
+// Sum of v over each row of 16 lanes, every lane of the row receiving it, in
+// a fixed order (quad swaps, then the half-row and row mirrors).
+constexpr int kDppQuadXor1 = 0xB1, kDppQuadXor2 = 0x4E, kDppRowHalfMirror = 0x141, kDppRowMirror = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __uint_as_float((uint32_t)__builtin_amdgcn_update_dpp(0, (int)__float_as_uint(v), CTRL, 0xf, 0xf, true));
+}
+
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f32<kDppQuadXor1>(v);
+  v += dpp_f32<kDppQuadXor2>(v);
+  v += dpp_f32<kDppRowHalfMirror>(v);
+  v += dpp_f32<kDppRowMirror>(v);
+  return v;
+}
+
 // Logit step of Algorithm 1 (section 3.3): with the candidates held constant,
 //   a_k = sum_i G_i w_hat^(B_k)_i + lambda B_k / n,
 //   dL/dl_k = (pi_k / tau) (a_k - sum_j pi_j a_j).
-// Same slab walk as the forward, with the gradients transposed through a
-// second LDS tile next to the weights (both slabs loaded coalesced and
-// prefetched a slab ahead); 34 KiB of LDS per wave leaves four resident
-// blocks per CU, so the grid is kGradBlocks.  sum_i G_i w_hat^(b)_i =
-// s_b sum_i G_i q_i, so each weight costs four FMAs.
+// Same slab walk as the forward.  The weights go through the LDS tile only for
+// the group statistics (lane per group, the quantizer's order); the scales go
+// to a small per-group table, and the products run in the coalesced layout of
+// the loads: lane l of load j holds weights and gradients 4(l%16) .. +3 of
+// group 4j + l/16, so the gradients never pass through LDS.  The four sums of
+// a group are reduced over its 16 lanes (fixed DPP order) and parked in the
+// padding of the group's tile row, where the lane that owns the group picks
+// them up.  The next slab's weights are loaded while this slab is worked on;
+// its gradients are loaded at the slab's start (a second gradient buffer
+// would cost the second wave per SIMD: 268 VGPRs, measured slower).
+// sum_i G_i w_hat^(b)_i = s_b sum_i G_i q_i.
 __global__ __launch_bounds__(64) void vbq_qat_grad_kernel(GradArgs a) {
-  __shared__ __attribute__((aligned(16))) float tile[2 * kGroupsPerSlab * kRowFloats];
+  __shared__ __attribute__((aligned(16))) float tile[kGroupsPerSlab * kRowFloats];
+  __shared__ __attribute__((aligned(16))) float consts[kGroupsPerSlab * 8];  // s1 s2 s4 s8 r2 r4 r8 -
   const uint32_t lane = threadIdx.x;
   const uint32_t base = (uint32_t)(size_t)(__attribute__((address_space(3))) float*)tile;
-  const TileAddr tw = tile_addr(base, lane);
-  const TileAddr tg = tile_addr(base + 4u * kGroupsPerSlab * kRowFloats, lane);
+  const uint32_t cbase = (uint32_t)(size_t)(__attribute__((address_space(3))) float*)consts;
+  const TileAddr ta = tile_addr(base, lane);
   const float pen1 = (float)((double)a.lambda * 1.0 / a.n_bbar), pen2 = (float)((double)a.lambda * 2.0 / a.n_bbar);
   const float pen4 = (float)((double)a.lambda * 4.0 / a.n_bbar), pen8 = (float)((double)a.lambda * 8.0 / a.n_bbar);
-
-  int64_t slab = blockIdx.x;
   const int64_t stride = gridDim.x;
-  u32x4 v[16], gv[16];
-  auto load_slab = [&](int64_t sl) {
+
+  u32x4 v[16];
+  auto load_slab = [&](int64_t sl) __attribute__((always_inline)) {
     const int64_t g0 = sl * kGroupsPerSlab;
     const int64_t left = a.n_groups - g0;
     const uint32_t ng = (uint32_t)(left < kGroupsPerSlab ? left : kGroupsPerSlab);
     const __amdgpu_buffer_rsrc_t rw = rsrc(a.W + g0 * 64, ng * 256u);
-    const __amdgpu_buffer_rsrc_t rg = rsrc(a.grad + g0 * 64, ng * 256u);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      v[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
-      gv[j] = __builtin_amdgcn_raw_buffer_load_b128(rg, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
-    }
+    for (int j = 0; j < 16; ++j) v[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
   };
-  if (slab < a.n_slabs) load_slab(slab);
 
-  for (; slab < a.n_slabs; slab += stride) {
-    const int64_t g0 = slab * kGroupsPerSlab;
+  // one slab: gv holds its gradients (coalesced, the weights' offsets); gn
+  // receives the next slab's
+  auto step = [&](int64_t sl) __attribute__((always_inline)) {
+    const int64_t g0 = sl * kGroupsPerSlab;
     const int64_t left = a.n_groups - g0;
     const uint32_t ng = (uint32_t)(left < kGroupsPerSlab ? left : kGroupsPerSlab);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      lds_store_u32x4(tw.co[j], v[j]);
-      lds_store_u32x4(tg.co[j], gv[j]);
-    }
+    for (int j = 0; j < 16; ++j) lds_store_u32x4(ta.co[j], v[j]);
     __syncthreads();
+    u32x4 gv[16];
+    const __amdgpu_buffer_rsrc_t rg = rsrc(a.grad + g0 * 64, ng * 256u);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) gv[j] = __builtin_amdgcn_raw_buffer_load_b128(rg, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
     const u32x4 pv = __builtin_amdgcn_raw_buffer_load_b128(rsrc(a.pi + g0 * 4, ng * 16u), (int)(lane * 16), 0, 0);
-    if (slab + stride < a.n_slabs) load_slab(slab + stride);
+    if (sl + stride < a.n_slabs) load_slab(sl + stride);
 
-    const Scales sc = group_scales(tw.row);
-    float d1 = 0.0f, d2 = 0.0f, d4 = 0.0f, d8 = 0.0f;  // sum_i G_i q_i per candidate
-#pragma unroll 2
+    // ---- scales of this lane's group, into the per-group table
+    const Scales own = group_scales(ta.row);
+    lds_store_u32x4(cbase + 32u * lane, u32x4{__float_as_uint(own.s1), __float_as_uint(own.c2.s),
+                                              __float_as_uint(own.c4.s), __float_as_uint(own.c8.s)});
+    lds_store_u32x4(cbase + 32u * lane + 16u, u32x4{__float_as_uint(own.c2.r), __float_as_uint(own.c4.r),
+                                                    __float_as_uint(own.c8.r), 0u});
+    __syncthreads();
+
+    // ---- products in the coalesced layout; sums of group 4j + lane/16 over its 16 lanes
+    // (fully unrolled: gv[j] must stay in registers)
+#pragma unroll
     for (int j = 0; j < 16; ++j) {
-      const u32x4 t = lds_u32x4(tw.row + 16u * j);
-      const u32x4 u = lds_u32x4(tg.row + 16u * j);
+      const uint32_t grp = 4u * j + (lane >> 4);
+      const u32x4 c0 = lds_u32x4(cbase + 32u * grp), c1 = lds_u32x4(cbase + 32u * grp + 16u);
+      Scales sc;
+      sc.s1 = __uint_as_float(c0.x);
+      sc.c2.s = __uint_as_float(c0.y);
+      sc.c4.s = __uint_as_float(c0.z);
+      sc.c8.s = __uint_as_float(c0.w);
+      sc.c2.r = __uint_as_float(c1.x);
+      sc.c4.r = __uint_as_float(c1.y);
+      sc.c8.r = __uint_as_float(c1.z);
+      sc.c2.qmax = 1.0f;
+      sc.c4.qmax = 7.0f;
+      sc.c8.qmax = 127.0f;
+      const u32x4 t = lds_u32x4(ta.co[j]);
       const float f[4] = {__uint_as_float(t.x), __uint_as_float(t.y), __uint_as_float(t.z), __uint_as_float(t.w)};
-      const float gr[4] = {__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w)};
+      const float gr[4] = {__uint_as_float(gv[j].x), __uint_as_float(gv[j].y), __uint_as_float(gv[j].z),
+                           __uint_as_float(gv[j].w)};
+      float d1 = 0.0f, d2 = 0.0f, d4 = 0.0f, d8 = 0.0f;  // sum G q per candidate, this lane's 4 weights
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float q2, q4, q8;
@@ -371,17 +414,35 @@ __global__ __launch_bounds__(64) void vbq_qat_grad_kernel(GradArgs a) {
         d4 = __builtin_fmaf(gr[i], q4, d4);
         d8 = __builtin_fmaf(gr[i], q8, d8);
       }
+      d1 = row16_sum(d1);
+      d2 = row16_sum(d2);
+      d4 = row16_sum(d4);
+      d8 = row16_sum(d8);
+      // the row's first lane parks the group's sums in the padding of the group's tile row
+      if ((lane & 15u) == 0)
+        lds_store_u32x4(base + 4u * (grp * kRowFloats + 64u),
+                        u32x4{__float_as_uint(d1), __float_as_uint(d2), __float_as_uint(d4), __float_as_uint(d8)});
     }
-    const float a1 = __builtin_fmaf(sc.s1, d1, pen1), a2 = __builtin_fmaf(sc.c2.s, d2, pen2);
-    const float a4 = __builtin_fmaf(sc.c4.s, d4, pen4), a8 = __builtin_fmaf(sc.c8.s, d8, pen8);
+    __syncthreads();
+
+    // ---- lane per group: the logit gradient of group g0 + lane
+    const u32x4 dv = lds_u32x4(ta.row + 256u);
+    const float a1 = __builtin_fmaf(own.s1, __uint_as_float(dv.x), pen1);
+    const float a2 = __builtin_fmaf(own.c2.s, __uint_as_float(dv.y), pen2);
+    const float a4 = __builtin_fmaf(own.c4.s, __uint_as_float(dv.z), pen4);
+    const float a8 = __builtin_fmaf(own.c8.s, __uint_as_float(dv.w), pen8);
     const float p0 = __uint_as_float(pv.x), p1 = __uint_as_float(pv.y), p2 = __uint_as_float(pv.z),
                 p3 = __uint_as_float(pv.w);
     const float mean = (p0 * a1 + p1 * a2) + (p2 * a4 + p3 * a8);
     const u32x4 out = {__float_as_uint(p0 / a.tau * (a1 - mean)), __float_as_uint(p1 / a.tau * (a2 - mean)),
                        __float_as_uint(p2 / a.tau * (a4 - mean)), __float_as_uint(p3 / a.tau * (a8 - mean))};
     __builtin_amdgcn_raw_buffer_store_b128(out, rsrc(a.dlogits + g0 * 4, ng * 16u), (int)(lane * 16), 0, 0);
-    __syncthreads();  // the next slab overwrites the tiles
-  }
+    __syncthreads();  // the next slab overwrites the tile and the table
+  };
+
+  int64_t slab = blockIdx.x;
+  if (slab < a.n_slabs) load_slab(slab);
+  for (; slab < a.n_slabs; slab += stride) step(slab);
 }
 
 // bbar = (sum of the per-block sums) / n_groups, summed in a fixed order.
