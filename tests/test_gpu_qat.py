@@ -347,3 +347,42 @@ def test_logit_grad_full_size(vbq):
     Gg = G.reshape(n, 64)[idx].reshape(-1)
     _check_grad(Wg, Gg, pi[idx], tau, lam, n, d[idx], "full size sampled")
     assert np.all(np.isfinite(d))
+
+
+# ------------------------------------------------------------ beyond 4 GiB
+
+BIG = (1 << 24) + (1 << 20) + 37  # 1.14G weights: every fp32 weight array passes the 4 GiB mark
+
+
+def _big_sample(n):
+    """Groups to check at full size: both sides of the 4 GiB byte offset, the ragged tail,
+    and random ones."""
+    edge = (1 << 32) // 256  # first group whose weights start at byte 2^32
+    rng = synth.rng_for(synth.SELECTION_SEED, 3006)
+    idx = np.concatenate([np.arange(edge - 70, edge + 70), np.arange(n - 100, n), rng.integers(0, n, size=3000)])
+    return np.unique(idx[(idx >= 0) & (idx < n)])
+
+
+def test_forward_beyond_4gib(vbq):
+    _say(f"qat forward n_groups={BIG} ({BIG * 256 / 2**30:.2f} GiB of weights)")
+    W, logits, noise = synth.selection_inputs(BIG, part=70_000)
+    tau = 0.7
+    w_soft, pi, hard, bbar = _run(vbq, W, logits, noise, tau)
+    idx = _big_sample(BIG)
+    _check_mix(W.reshape(BIG, 64)[idx].reshape(-1), logits[idx], noise[idx], tau, w_soft.reshape(BIG, 64)[idx],
+               pi[idx], None, "beyond 4 GiB sampled")
+    np.testing.assert_array_equal(hard, oqat.harden(logits.reshape(BIG, 1, 4)).reshape(BIG))
+    pi_ref = oqat.gumbel_softmax(logits, noise, tau)
+    bbar_ref = float(np.sum(pi_ref * WIDTHS) / BIG)
+    assert abs(float(bbar[0]) - bbar_ref) <= (float(_eps(logits, noise, tau).max()) + 8 * U) * bbar_ref
+
+
+def test_logit_grad_beyond_4gib(vbq):
+    _say(f"qat logit grad n_groups={BIG}")
+    tau, lam = 0.7, 0.01
+    W, G, pi = _grad_inputs(BIG, 71_000, tau)
+    d = vbq.qat_logit_grad(_dev(W), _dev(G), _dev(pi), tau, lam).cpu().numpy()
+    idx = _big_sample(BIG)
+    _check_grad(W.reshape(BIG, 64)[idx].reshape(-1), G.reshape(BIG, 64)[idx].reshape(-1), pi[idx], tau, lam, BIG,
+                d[idx], "beyond 4 GiB sampled")
+    assert np.all(np.isfinite(d))
