@@ -1,7 +1,9 @@
 // Differentiable bit selection on gfx950 (MI355X): the forward pass of the
-// selection path of paper section 3.2 and Algorithm 1.
+// selection path (paper section 3.2, Algorithm 1) and the gradient of its
+// logit step (section 3.3); the gradient kernel is described where it is
+// defined.
 //
-// For every group g of 64 contiguous weights the kernel forms the four
+// For every group g of 64 contiguous weights the forward kernel forms the four
 // candidate reconstructions w_hat^(b), b in {1, 2, 4, 8} (section 3.1: Eq. (1)
 // for b >= 2, sign times absmean for b = 1), the Gumbel-Softmax weights
 // pi_g = softmax((l_g + e_g) / tau), and the soft weight
@@ -359,8 +361,8 @@ __global__ __launch_bounds__(64) void vbq_qat_grad_kernel(GradArgs a) {
     for (int j = 0; j < 16; ++j) v[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
   };
 
-  // one slab: gv holds its gradients (coalesced, the weights' offsets); gn
-  // receives the next slab's
+  // one slab; its gradients are loaded at its start, coalesced, at the
+  // weights' offsets
   auto step = [&](int64_t sl) __attribute__((always_inline)) {
     const int64_t g0 = sl * kGroupsPerSlab;
     const int64_t left = a.n_groups - g0;

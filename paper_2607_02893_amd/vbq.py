@@ -227,6 +227,23 @@ def _stream_handle(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _need(t, name, dtype, numel=None, device=None, min_numel=None):
+    """A device tensor the kernels may read or write: on a GPU (a host pointer
+    would fault in a kernel), of the given dtype, contiguous and of the given
+    size (exact, or at least min_numel), on `device` when given."""
+    if t is None or not getattr(t, "is_cuda", False):
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} must have {numel} elements, not {t.numel()}")
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError(f"{name} must have at least {min_numel} elements")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    return t
+
+
 class PackedMatrix:
     """A packed matrix resident in device memory (torch uint8 tensor) plus its descriptor."""
 
@@ -247,10 +264,11 @@ class PackedMatrix:
     def gemv(self, x, y=None, stream=None):
         """y[N] (float32) = w_hat @ x, x a contiguous fp16 device tensor of length K."""
         import torch
-        if x.dtype != torch.float16 or not x.is_contiguous() or x.numel() != self.K:
-            raise ValueError("x must be a contiguous float16 tensor of length K")
+        dev = self.blob.device
+        _need(x, "x", torch.float16, self.K, dev)
         if y is None:
-            y = torch.empty(self.N, dtype=torch.float32, device=x.device)
+            y = torch.empty(self.N, dtype=torch.float32, device=dev)
+        _need(y, "y", torch.float32, self.N, dev)
         _check(_lib.vbq_gemv(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()),
                              ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()),
                              _stream_handle(stream)), "vbq_gemv")
@@ -260,12 +278,10 @@ class PackedMatrix:
         """y[rows[n]] = (w_hat @ x)[n] for every n (indices outside y are not written): one row
         bucket of a bucketed matrix.  y: float32 device tensor; rows: int32 device tensor of length N."""
         import torch
-        if x.dtype != torch.float16 or not x.is_contiguous() or x.numel() != self.K:
-            raise ValueError("x must be a contiguous float16 tensor of length K")
-        if y.dtype != torch.float32 or not y.is_contiguous():
-            raise ValueError("y must be a contiguous float32 tensor")
-        if rows.dtype != torch.int32 or not rows.is_contiguous() or rows.numel() != self.N:
-            raise ValueError("rows must be a contiguous int32 tensor of length N")
+        dev = self.blob.device
+        _need(x, "x", torch.float16, self.K, dev)
+        _need(y, "y", torch.float32, None, dev)
+        _need(rows, "rows", torch.int32, self.N, dev)
         _check(_lib.vbq_gemv_rows(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()),
                                   ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()), y.numel(),
                                   ctypes.c_void_p(rows.data_ptr()), _stream_handle(stream)), "vbq_gemv_rows")
@@ -274,11 +290,17 @@ class PackedMatrix:
     def gemm_small(self, X, Y=None, stream=None):
         """Y[M][N] (float32) = X @ w_hat^T for an fp16 device tensor X[M][K], M <= 16."""
         import torch
+        dev = self.blob.device
+        if not getattr(X, "is_cuda", False) or X.device != dev:
+            raise ValueError(f"X must be a GPU tensor on {dev}")
         if X.dtype != torch.float16 or X.dim() != 2 or X.shape[1] != self.K or X.stride(1) != 1:
             raise ValueError("X must be a float16 [M, K] tensor with unit column stride")
         M = X.shape[0]
         if Y is None:
-            Y = torch.empty((M, self.N), dtype=torch.float32, device=X.device)
+            Y = torch.empty((M, self.N), dtype=torch.float32, device=dev)
+        if (not getattr(Y, "is_cuda", False) or Y.device != dev or Y.dtype != torch.float32 or Y.dim() != 2
+                or Y.shape[0] != M or Y.shape[1] != self.N or Y.stride(1) != 1):
+            raise ValueError(f"Y must be a float32 [M, N] GPU tensor on {dev} with unit column stride")
         _check(_lib.vbq_gemm_small(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()), M,
                                    ctypes.c_void_p(X.data_ptr()), X.stride(0), ctypes.c_void_p(Y.data_ptr()),
                                    Y.stride(0), _stream_handle(stream)), "vbq_gemm_small")
@@ -289,6 +311,7 @@ class PackedMatrix:
         import torch
         if W is None:
             W = torch.empty((self.N, self.K), dtype=torch.float32, device=self.blob.device)
+        _need(W, "W", torch.float32, self.N * self.K, self.blob.device)
         _check(_lib.vbq_dequant(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()),
                                 ctypes.c_void_p(W.data_ptr()), _stream_handle(stream)), "vbq_dequant")
         return W
@@ -313,8 +336,10 @@ class BucketedMatrix:
     def gemv(self, x, y=None, stream=None):
         """y[N] (float32) = w_hat @ x: one vbq_gemv_rows per bucket, on one stream."""
         import torch
+        dev = self.parts[0][1].blob.device
         if y is None:
-            y = torch.empty(self.N, dtype=torch.float32, device=x.device)
+            y = torch.empty(self.N, dtype=torch.float32, device=dev)
+        _need(y, "y", torch.float32, self.N, dev)
         for _, Wp, rows in self.parts:
             Wp.gemv_rows(x, y, rows, stream)
         return y
@@ -346,15 +371,17 @@ def qat_forward(W, logits, noise, tau, w_soft=None, pi=True, hard_bits=True, bba
     element (None where skipped).
     """
     import torch
-    if W.dtype != torch.float32 or not W.is_contiguous() or W.numel() % 64:
-        raise ValueError("W must be a contiguous float32 tensor with a multiple of 64 elements")
+    _need(W, "W", torch.float32)
+    if W.numel() % 64:
+        raise ValueError("W must have a multiple of 64 elements")
     n = W.numel() // 64
-    for name, t in (("logits", logits), ("noise", noise)):
-        if t is not None and (t.dtype != torch.float32 or not t.is_contiguous() or t.numel() != 4 * n):
-            raise ValueError(f"{name} must be a contiguous float32 tensor of n_groups*4 elements")
     dev = W.device
+    _need(logits, "logits", torch.float32, 4 * n, dev)
+    if noise is not None:
+        _need(noise, "noise", torch.float32, 4 * n, dev)
     if w_soft is None:
         w_soft = torch.empty_like(W)
+    _need(w_soft, "w_soft", torch.float32, W.numel(), dev)
     if pi is True:
         pi = torch.empty((n, 4), dtype=torch.float32, device=dev)
     if hard_bits is True:
@@ -364,11 +391,17 @@ def qat_forward(W, logits, noise, tau, w_soft=None, pi=True, hard_bits=True, bba
     pi = pi if pi is not False else None
     hard_bits = hard_bits if hard_bits is not False else None
     bbar = bbar if bbar is not False else None
+    if pi is not None:
+        _need(pi, "pi", torch.float32, 4 * n, dev)
+    if hard_bits is not None:
+        _need(hard_bits, "hard_bits", torch.uint8, n, dev)
     ws_bytes = 0
     if bbar is not None:
+        _need(bbar, "bbar", torch.float64, None, dev, min_numel=1)
         ws_bytes = qat_workspace_size(n)
         if workspace is None:
             workspace = torch.empty(max(ws_bytes, 8), dtype=torch.uint8, device=dev)
+        _need(workspace, "workspace", workspace.dtype, None, dev)
         ws_bytes = workspace.numel() * workspace.element_size()
     _check(_lib.vbq_qat_forward(n, _dev_ptr(W), _dev_ptr(logits), _dev_ptr(noise), float(tau), _dev_ptr(w_soft),
                                 _dev_ptr(pi), _dev_ptr(hard_bits), _dev_ptr(bbar), _dev_ptr(workspace), ws_bytes,
@@ -385,14 +418,16 @@ def qat_logit_grad(W, grad, pi, tau, lam, n_bbar=None, dlogits=None, stream=None
     [n_groups, 4].
     """
     import torch
-    for name, t, k in (("W", W, 64), ("grad", grad, 64), ("pi", pi, 4)):
-        if t.dtype != torch.float32 or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous float32 tensor")
+    _need(W, "W", torch.float32)
+    if W.numel() % 64:
+        raise ValueError("W must have a multiple of 64 elements")
     n = W.numel() // 64
-    if W.numel() % 64 or grad.numel() != W.numel() or pi.numel() != 4 * n:
-        raise ValueError("W and grad need n_groups*64 elements and pi n_groups*4")
+    dev = W.device
+    _need(grad, "grad", torch.float32, W.numel(), dev)
+    _need(pi, "pi", torch.float32, 4 * n, dev)
     if dlogits is None:
-        dlogits = torch.empty((n, 4), dtype=torch.float32, device=W.device)
+        dlogits = torch.empty((n, 4), dtype=torch.float32, device=dev)
+    _need(dlogits, "dlogits", torch.float32, 4 * n, dev)
     _check(_lib.vbq_qat_logit_grad(n, _dev_ptr(W), _dev_ptr(grad), _dev_ptr(pi), float(tau), float(lam),
                                    int(n if n_bbar is None else n_bbar), _dev_ptr(dlogits), _stream_handle(stream)),
            "vbq_qat_logit_grad")

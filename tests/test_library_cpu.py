@@ -314,3 +314,16 @@ def test_qat_logit_grad_argument_errors():
     assert f(4, A + 4, A, A, 1.0, 0.5, 4, A, 0) == 7               # misaligned
     assert f(4, A, A, A + 8, 1.0, 0.5, 4, A, 0) == 7
     assert f(4, A, A, A, 1.0, 0.5, 4, A + 4, 0) == 7
+
+
+def test_binding_rejects_host_tensors_and_wrong_outputs():
+    # a host pointer in a kernel would fault: the binding refuses before any call
+    torch = pytest.importorskip("torch")
+    W = torch.zeros(128)
+    l = torch.zeros(8)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        vbq.qat_forward(W, l, None, 1.0)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        vbq.qat_logit_grad(W, torch.zeros(128), torch.zeros(8), 1.0, 0.1)
+    with pytest.raises(ValueError):
+        vbq._need(torch.zeros(3, dtype=torch.float16), "x", torch.float16, 3)
