@@ -385,6 +385,20 @@ def main_qat(args):
     # the forward kernel alone, K launches back to back on the same stream
     _, kern_s = timed(lambda: fwd(False), args.steps)
     log(f"forward kernel alone: {1e6 * kern_s:.1f} us per launch")
+    # the same forward writing w_soft as bf16 (6 bytes per weight instead of 8)
+    ws16 = torch.empty(n * 64, dtype=torch.bfloat16, device=dev)
+
+    def fwd16():
+        st = vbq.raw_qat_forward(n, Wd.data_ptr(), ld.data_ptr(), nd.data_ptr(), tau, ws16.data_ptr(), pi.data_ptr(),
+                                 hard.data_ptr(), 0, 0, 0, sptr, flags=vbq.QAT_WSOFT_BF16)
+        if st != 0:
+            raise vbq.VbqError(st, "vbq_qat_forward (bf16)")
+    for _ in range(3):
+        fwd16()
+    _, k16_s = timed(fwd16, args.steps)
+    alg16 = alg_kernel - n * 64 * 2
+    log(f"forward kernel, bf16 w_soft: {1e6 * k16_s:.1f} us per launch, {alg16 / k16_s / 1e9:.0f} GB/s")
+    del ws16
     # the logit step's gradient (Algorithm 1, every m-th step): same weights, a
     # seeded dL/dw_soft, the forward's pi
     grad = torch.from_numpy(synth.rng_for(synth.SELECTION_SEED, 3004, 1).standard_normal(
@@ -447,6 +461,10 @@ def main_qat(args):
                      "timing": "HIP events on the launch stream around K launches of the kernel alone",
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "traffic_vs_algorithmic": round(traffic / alg_kernel, 3) if traffic else None},
+        "w_soft_bf16": {"kernel": "vbq_qat_forward_kernel<bf16>", "us_per_launch": round(1e6 * k16_s, 2),
+                        "algorithmic_bytes": int(alg16), "GBps": round(alg16 / k16_s / 1e9, 1),
+                        "frac": round(alg16 / k16_s / 1e9 / PEAK_HBM_GBS, 4),
+                        "note": "the same forward writing w_soft as bf16 (rounded to nearest even)"},
         "logit_grad": {"kernel": "vbq_qat_grad_kernel", "us_per_launch": round(1e6 * grad_s, 2),
                        "algorithmic_bytes": int(alg_grad), "GBps": round(alg_grad / grad_s / 1e9, 1),
                        "frac": round(alg_grad / grad_s / 1e9 / PEAK_HBM_GBS, 4),

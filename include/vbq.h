@@ -218,6 +218,9 @@ vbq_status vbq_dequant(const vbq_desc* desc, const void* blob_dev,
  * ------------------------------------------------------------------------- */
 
 #define VBQ_QAT_MAX_GROUPS (((int64_t)1) << 40)
+/* vbq_qat_forward flag: write w_soft as bf16 (each fp32 result rounded to
+ * nearest even) instead of float. */
+#define VBQ_QAT_WSOFT_BF16 1u
 
 /* Bytes of device workspace vbq_qat_forward needs to compute bbar for
  * n_groups groups (8 bytes per block of its launch).  VBQ_ERR_NULL or
@@ -246,8 +249,11 @@ vbq_status vbq_qat_workspace_size(int64_t n_groups, size_t* bytes);
  *   noise_dev    float[n_groups][4] Gumbel noise drawn by the caller, 16-byte
  *                aligned, or NULL for no noise (plain softmax).
  *   tau          temperature, finite and > 0.
- *   w_soft_dev   float[n_groups*64] output, 16-byte aligned; may not overlap
- *                the inputs.
+ *   flags        0, or VBQ_QAT_WSOFT_BF16 for a bf16 w_soft; other bits give
+ *                VBQ_ERR_UNSUPPORTED.
+ *   w_soft_dev   float[n_groups*64] output (bf16[n_groups*64] with
+ *                VBQ_QAT_WSOFT_BF16), 16-byte aligned; may not overlap the
+ *                inputs.
  *   pi_dev       float[n_groups][4] output (16-byte aligned) or NULL.
  *   hard_bits_dev uint8[n_groups] output or NULL.
  *   bbar_dev     one double output (8-byte aligned) or NULL; needs a workspace
@@ -257,14 +263,15 @@ vbq_status vbq_qat_workspace_size(int64_t n_groups, size_t* bytes);
  * n_groups == 0 does nothing (any pointer may then be NULL; bbar is not
  * written).  Errors: VBQ_ERR_NULL (W, logits or w_soft NULL; workspace NULL
  * with bbar), VBQ_ERR_SHAPE (n_groups out of range),
- * VBQ_ERR_NONFINITE (tau NaN/Inf), VBQ_ERR_UNSUPPORTED (tau <= 0),
- * VBQ_ERR_BUFFER (misaligned pointer or workspace too small), VBQ_ERR_HIP. */
+ * VBQ_ERR_NONFINITE (tau NaN/Inf), VBQ_ERR_UNSUPPORTED (tau <= 0, unknown
+ * flags), VBQ_ERR_BUFFER (misaligned pointer or workspace too small),
+ * VBQ_ERR_HIP. */
 vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev,
                            const float* logits_dev, const float* noise_dev,
-                           float tau, float* w_soft_dev, float* pi_dev,
-                           uint8_t* hard_bits_dev, double* bbar_dev,
-                           void* workspace_dev, size_t workspace_bytes,
-                           void* stream);
+                           float tau, uint32_t flags, void* w_soft_dev,
+                           float* pi_dev, uint8_t* hard_bits_dev,
+                           double* bbar_dev, void* workspace_dev,
+                           size_t workspace_bytes, void* stream);
 
 /* Gradient of the logit step (paper section 3.3, "Gradient isolation", and
  * Algorithm 1): the candidate reconstructions are held constant, so with

@@ -44,6 +44,8 @@ vbq_status vbq_detail_hip_status(hipError_t e);
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kGroupsPerSlab = 64;  // one group per lane
 constexpr int kRowFloats = 68;      // LDS row of one group: 64 weights + 4 floats of padding
@@ -179,7 +181,7 @@ struct QatArgs {
   const float* W;
   const float* logits;
   const float* noise;  // may be null
-  float* w_soft;
+  void* w_soft;        // float, or bf16 with kBf16
   float* pi;           // may be null
   uint8_t* hard;       // may be null
   double* partial;     // per-block sums of sum_k pi_k B_k, or null
@@ -188,6 +190,13 @@ struct QatArgs {
   int64_t n_slabs;
 };
 
+// Two fp32 values as a bf16 pair, each rounded to nearest even (one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
+  const bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+template <bool kBf16>
 __global__ __launch_bounds__(64) void vbq_qat_forward_kernel(QatArgs a) {
   __shared__ __attribute__((aligned(16))) float tile[kGroupsPerSlab * kRowFloats];
   const uint32_t lane = threadIdx.x;
@@ -281,11 +290,23 @@ __global__ __launch_bounds__(64) void vbq_qat_forward_kernel(QatArgs a) {
       lds_store_u32x4(row_addr + 16u * j, o);
     }
 
-    // ---- out of LDS with coalesced stores
+    // ---- out of LDS with coalesced stores (bf16: each float rounded to nearest even)
     __syncthreads();
-    const __amdgpu_buffer_rsrc_t ro = rsrc(a.w_soft + g0 * 64, ng * 256u);
+    if constexpr (kBf16) {
+      const __amdgpu_buffer_rsrc_t ro = rsrc((const uint16_t*)a.w_soft + g0 * 64, ng * 128u);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) __builtin_amdgcn_raw_buffer_store_b128(lds_u32x4(co_addr[j]), ro, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
+      for (int j = 0; j < 16; ++j) {
+        const u32x4 t = lds_u32x4(co_addr[j]);
+        const u32x2 o = {bf16_pair(__uint_as_float(t.x), __uint_as_float(t.y)),
+                         bf16_pair(__uint_as_float(t.z), __uint_as_float(t.w))};
+        __builtin_amdgcn_raw_buffer_store_b64(o, ro, (int)(j * 512 + lane * 8), 0, kNonTemporal);
+      }
+    } else {
+      const __amdgpu_buffer_rsrc_t ro = rsrc((const float*)a.w_soft + g0 * 64, ng * 256u);
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+        __builtin_amdgcn_raw_buffer_store_b128(lds_u32x4(co_addr[j]), ro, (int)(j * 1024 + lane * 16), 0, kNonTemporal);
+    }
     __syncthreads();  // the next slab overwrites the tile
   }
 
@@ -481,11 +502,12 @@ vbq_status vbq_qat_workspace_size(int64_t n_groups, size_t* bytes) {
 }
 
 vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev, const float* logits_dev, const float* noise_dev,
-                           float tau, float* w_soft_dev, float* pi_dev, uint8_t* hard_bits_dev, double* bbar_dev,
-                           void* workspace_dev, size_t workspace_bytes, void* stream) {
+                           float tau, uint32_t flags, void* w_soft_dev, float* pi_dev, uint8_t* hard_bits_dev,
+                           double* bbar_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
   if (n_groups < 0 || n_groups > VBQ_QAT_MAX_GROUPS) return VBQ_ERR_SHAPE;
   if (!(tau == tau) || tau == __builtin_inff() || tau == -__builtin_inff()) return VBQ_ERR_NONFINITE;
   if (!(tau > 0.0f)) return VBQ_ERR_UNSUPPORTED;
+  if (flags & ~VBQ_QAT_WSOFT_BF16) return VBQ_ERR_UNSUPPORTED;
   if (n_groups == 0) return VBQ_OK;
   if (!W_dev || !logits_dev || !w_soft_dev) return VBQ_ERR_NULL;
   if (!aligned(W_dev, 16) || !aligned(logits_dev, 16) || !aligned(w_soft_dev, 16) ||
@@ -510,8 +532,9 @@ vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev, const float* lo
   a.n_groups = n_groups;
   a.n_slabs = (n_groups + kGroupsPerSlab - 1) / kGroupsPerSlab;
   void* args[] = {&a};
-  vbq_status st = vbq_detail_hip_status(
-      hipLaunchKernel((const void*)vbq_qat_forward_kernel, dim3((unsigned)blocks), dim3(64), args, 0, s));
+  const void* kernel = (flags & VBQ_QAT_WSOFT_BF16) ? (const void*)vbq_qat_forward_kernel<true>
+                                                    : (const void*)vbq_qat_forward_kernel<false>;
+  vbq_status st = vbq_detail_hip_status(hipLaunchKernel(kernel, dim3((unsigned)blocks), dim3(64), args, 0, s));
   if (st != VBQ_OK || !bbar_dev) return st;
   const double* part = (const double*)workspace_dev;
   int n = (int)blocks;

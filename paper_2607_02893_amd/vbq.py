@@ -58,6 +58,7 @@ EXPORTS = ("vbq_status_string", "vbq_last_hip_error", "vbq_layout_version", "vbq
            "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_gemm_small", "vbq_dequant",
            "vbq_qat_workspace_size", "vbq_qat_forward", "vbq_qat_logit_grad")
 QAT_MAX_GROUPS = 1 << 40
+QAT_WSOFT_BF16 = 1
 QAT_CANDIDATES = (1, 2, 4, 8)
 
 
@@ -114,7 +115,8 @@ _lib.vbq_dequant.argtypes = [ctypes.POINTER(VbqDesc), _P, _P, _P]
 _lib.vbq_qat_workspace_size.restype = ctypes.c_int
 _lib.vbq_qat_workspace_size.argtypes = [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]
 _lib.vbq_qat_forward.restype = ctypes.c_int
-_lib.vbq_qat_forward.argtypes = [ctypes.c_int64, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.vbq_qat_forward.argtypes = [ctypes.c_int64, _P, _P, _P, ctypes.c_float, ctypes.c_uint32, _P, _P, _P, _P, _P,
+                                 ctypes.c_size_t, _P]
 _lib.vbq_qat_logit_grad.restype = ctypes.c_int
 _lib.vbq_qat_logit_grad.argtypes = [ctypes.c_int64, _P, _P, _P, ctypes.c_float, ctypes.c_float, ctypes.c_int64, _P, _P]
 
@@ -359,14 +361,16 @@ def _dev_ptr(t):
 
 
 def qat_forward(W, logits, noise, tau, w_soft=None, pi=True, hard_bits=True, bbar=True, workspace=None,
-                stream=None):
+                stream=None, w_soft_dtype=None):
     """Forward pass of the selection path (paper section 3.2, Algorithm 1) on device tensors.
 
     W: contiguous float32 device tensor whose numel is a multiple of 64 (its
     groups are consecutive runs of 64; a row-major [N, K] matrix with K % 64 == 0
     qualifies).  logits / noise: contiguous float32 [n_groups, 4] (any shape of
     that size); noise may be None.  pi / hard_bits / bbar: True to allocate the
-    output, a tensor to write into, or False/None to skip it.  Returns
+    output, a tensor to write into, or False/None to skip it.  w_soft is float32,
+    or bfloat16 (each value rounded to nearest even) when w_soft_dtype or the
+    given w_soft tensor says so.  Returns
     (w_soft, pi, hard_bits, bbar) with bbar a float64 device tensor of one
     element (None where skipped).
     """
@@ -379,9 +383,14 @@ def qat_forward(W, logits, noise, tau, w_soft=None, pi=True, hard_bits=True, bba
     _need(logits, "logits", torch.float32, 4 * n, dev)
     if noise is not None:
         _need(noise, "noise", torch.float32, 4 * n, dev)
+    if w_soft_dtype is None:
+        w_soft_dtype = torch.float32 if w_soft is None else w_soft.dtype
+    if w_soft_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("w_soft must be float32 or bfloat16")
     if w_soft is None:
-        w_soft = torch.empty_like(W)
-    _need(w_soft, "w_soft", torch.float32, W.numel(), dev)
+        w_soft = torch.empty(W.shape, dtype=w_soft_dtype, device=dev)
+    _need(w_soft, "w_soft", w_soft_dtype, W.numel(), dev)
+    flags = QAT_WSOFT_BF16 if w_soft_dtype == torch.bfloat16 else 0
     if pi is True:
         pi = torch.empty((n, 4), dtype=torch.float32, device=dev)
     if hard_bits is True:
@@ -403,7 +412,7 @@ def qat_forward(W, logits, noise, tau, w_soft=None, pi=True, hard_bits=True, bba
             workspace = torch.empty(max(ws_bytes, 8), dtype=torch.uint8, device=dev)
         _need(workspace, "workspace", workspace.dtype, None, dev)
         ws_bytes = workspace.numel() * workspace.element_size()
-    _check(_lib.vbq_qat_forward(n, _dev_ptr(W), _dev_ptr(logits), _dev_ptr(noise), float(tau), _dev_ptr(w_soft),
+    _check(_lib.vbq_qat_forward(n, _dev_ptr(W), _dev_ptr(logits), _dev_ptr(noise), float(tau), flags, _dev_ptr(w_soft),
                                 _dev_ptr(pi), _dev_ptr(hard_bits), _dev_ptr(bbar), _dev_ptr(workspace), ws_bytes,
                                 _stream_handle(stream)), "vbq_qat_forward")
     return w_soft, pi, hard_bits, bbar
@@ -442,10 +451,11 @@ def raw_qat_logit_grad(n_groups, W_ptr, grad_ptr, pi_ptr, tau, lam, n_bbar, d_pt
 
 
 def raw_qat_forward(n_groups, W_ptr, logits_ptr, noise_ptr, tau, w_soft_ptr, pi_ptr, hard_ptr, bbar_ptr,
-                    ws_ptr, ws_bytes, stream_ptr):
+                    ws_ptr, ws_bytes, stream_ptr, flags=0):
     """vbq_qat_forward on raw device addresses (0 for NULL)."""
     v = lambda p: ctypes.c_void_p(p) if p else None  # noqa: E731
-    return _lib.vbq_qat_forward(int(n_groups), v(W_ptr), v(logits_ptr), v(noise_ptr), float(tau), v(w_soft_ptr),
+    return _lib.vbq_qat_forward(int(n_groups), v(W_ptr), v(logits_ptr), v(noise_ptr), float(tau), int(flags),
+                                v(w_soft_ptr),
                                 v(pi_ptr), v(hard_ptr), v(bbar_ptr), v(ws_ptr), int(ws_bytes), v(stream_ptr))
 
 

@@ -386,3 +386,41 @@ def test_logit_grad_beyond_4gib(vbq):
     _check_grad(W.reshape(BIG, 64)[idx].reshape(-1), G.reshape(BIG, 64)[idx].reshape(-1), pi[idx], tau, lam, BIG,
                 d[idx], "beyond 4 GiB sampled")
     assert np.all(np.isfinite(d))
+
+
+# ------------------------------------------------------------- bf16 w_soft
+
+@pytest.mark.parametrize("n", [1, 65, 4097, 2 * 64 * 2048 + 77])
+def test_bf16_w_soft_is_the_rounded_fp32_result(vbq, n):
+    # the bf16 output is the fp32 result rounded to nearest even (torch's CPU conversion
+    # is the reference rounding), and so within the fp32 bound plus half a bf16 ulp
+    _say(f"qat forward bf16 n_groups={n}")
+    W, logits, noise = synth.selection_inputs(n, part=80_000 + n)
+    tau = 0.5
+    w32 = _run(vbq, W, logits, noise, tau)[0]
+    out = vbq.qat_forward(_dev(W), _dev(logits), _dev(noise), tau, w_soft_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    w16 = out[0]
+    assert w16.dtype == torch.bfloat16
+    want = torch.from_numpy(w32).to(torch.bfloat16)
+    assert torch.equal(w16.cpu().view(torch.int16), want.view(torch.int16))
+    ref = oqat.forward(W.reshape(n, 64).astype(np.float64), logits.reshape(n, 1, 4), noise.reshape(n, 1, 4), tau)
+    cand = oqat.candidates(W.reshape(n, 64).astype(np.float64)).reshape(4, n, 64)
+    A = np.einsum("gk,kgi->gi", ref["pi"].reshape(n, 4), np.abs(cand))
+    eps = _eps(logits, noise, tau)
+    got = w16.float().cpu().numpy().reshape(n, 64).astype(np.float64)
+    exact = ref["w_soft"].reshape(n, 64)
+    bound = (eps[:, None] + 8 * U) * A * (1 + 2.0 ** -8) + 2.0 ** -8 * np.abs(exact) + 1e-37 * cand.__abs__().sum(0)
+    assert np.all(np.abs(got - exact) <= bound)
+
+
+def test_bf16_one_hot_is_the_rounded_candidate(vbq):
+    n = 5000
+    W, _, _ = synth.selection_inputs(n, part=90_000)
+    widx = synth.rng_for(synth.SELECTION_SEED, 3007).integers(0, 4, size=n)
+    out = vbq.qat_forward(_dev(W), _dev(_one_hot_logits(widx)), None, 0.5, w_soft_dtype=torch.bfloat16, pi=False,
+                          hard_bits=False, bbar=False)
+    cand = oqat.candidates(W.reshape(n, 64).astype(np.float64)).reshape(4, n, 64)[widx, np.arange(n)]
+    want = torch.from_numpy(cand.astype(np.float32)).to(torch.bfloat16)  # exact in fp32, then rounded once
+    # values compared (a zero candidate of a negative weight may come out as -0.0)
+    assert torch.equal(out[0].cpu().reshape(n, 64), want)

@@ -296,6 +296,8 @@ def test_qat_forward_argument_errors():
     assert f(4, A, A, 0, 1.0, A, 0, 0, A, A + 4, 8, 0) == 7        # workspace misaligned
     assert f(100, A, A, 0, 1.0, A, 0, 0, A, A, 8, 0) == 7          # workspace too small (needs 16)
     assert f(0, A, A, 0, 1.0, A, 0, 0, A, A, 0, 0) == 0            # empty: workspace of 0 bytes is enough
+    assert f(4, A, A, 0, 1.0, A, 0, 0, 0, 0, 0, 0, flags=2) == 10  # unknown flag
+    assert f(4, A, A, 0, 1.0, A + 8, 0, 0, 0, 0, 0, 0, flags=1) == 7  # bf16 w_soft misaligned
 
 
 def test_qat_logit_grad_argument_errors():
