@@ -637,6 +637,22 @@ def main():
     except Exception as e:  # graph capture is an optimisation of the same launches
         log(f"graph capture unavailable: {e}")
 
+    # the distribution of single steps (each bracketed by its own events; the
+    # timed region above gives the mean)
+    run_one = g.replay if graph_s is not None and graph_s <= eager_s else step
+    n_dist = min(100, args.steps)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_dist)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        run_one()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    st_us = np.array([e0.elapsed_time(e1) * 1e3 for e0, e1 in ev])
+    step_dist = {"median": round(float(np.median(st_us)), 2), "p10": round(float(np.percentile(st_us, 10)), 2),
+                 "p90": round(float(np.percentile(st_us, 90)), 2), "steps": n_dist,
+                 "timing": "HIP events around each step, on the launch stream"}
+    log(f"single steps: median {step_dist['median']} us, p10 {step_dist['p10']}, p90 {step_dist['p90']}")
+
     # cold steps: every byte of the step comes from HBM (small workloads
     # otherwise stay resident in the 256 MB Infinity Cache between steps)
     cold_us = None
@@ -761,6 +777,7 @@ def main():
         "us_per_step_eager": round(1e6 * eager_s, 2),
         "us_per_step_graph": round(1e6 * graph_s, 2) if graph_s is not None else None,
         "us_per_step_cold": cold_us,
+        "us_per_step_distribution": step_dist,
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
