@@ -362,3 +362,25 @@ def test_recipe_workload_full_size(vbq):
                        what="recipe head")
     assert np.all(np.isfinite(y))
     _say(f"recipe head {head.N}x{head.K} (4 buckets): max rel err {rel:.2e}")
+
+
+@pytest.mark.parametrize("N,K", [(33, 1 << 20), ((1 << 20) + 3, 64)])
+def test_extreme_aspect_ratios(vbq, N, K):
+    # a very wide matrix (16384 group columns, a ragged 33-row tile) and a very tall one
+    # (one group column, 2^20 + 3 rows): every row checked against the oracle, GEMV and M = 4
+    _say(f"extreme shape N={N} K={K}")
+    spec = synth.MatrixSpec("t", 0, 0, N, K)
+    bits, q, s = synth.make_matrix(spec, 53)
+    Wp = _packed(vbq, q, s, bits)
+    X = synth.make_x(spec, 53, M=4)
+    y = Wp.gemv(_x_dev(X[0])).cpu().numpy()
+    parity.check(y, omatmul.gemv(q, s, X[0]), omatmul.row_magnitude(q, s, X[0]), what=f"gemv {N}x{K}")
+    Y = Wp.gemm_small(_x_dev(X)).cpu().numpy()
+    for m in range(4):
+        parity.check(Y[m], omatmul.gemv(q, s, X[m]), omatmul.row_magnitude(q, s, X[m]), what=f"M=4 row {m}")
+    if N < 64:  # one-hot columns of the wide matrix, including the last group column
+        W = omatmul.dequant(q, s)
+        for k in (0, 64 * 8191 + 5, K - 1):
+            e = np.zeros(K, dtype=np.float16)
+            e[k] = 1.0
+            assert np.array_equal(Wp.gemv(_x_dev(e)).cpu().numpy().astype(np.float64), W[:, k]), k
