@@ -188,7 +188,9 @@ vbq_status vbq_gemv(const vbq_desc* desc, const void* blob_dev,
  * row n of this matrix is written to y_dev[row_index_dev[n]]: a bucket is
  * packed as its own matrix (one width, so no width map) and called with the
  * output rows of its members.  row_index_dev: device int32[N]; an index
- * outside [0, y_len) is not written (no error).  The caller owns every buffer;
+ * outside [0, y_len) is not written (no error).  The indices of one call
+ * should be distinct: rows sharing an index are all written to it, in no
+ * defined order (the value is one of theirs).  The caller owns every buffer;
  * buckets of one output may run back to back on one stream.  Errors: NULL,
  * SHAPE (y_len < 0), BUFFER (misaligned pointers), DESC, HIP. */
 vbq_status vbq_gemv_rows(const vbq_desc* desc, const void* blob_dev,
