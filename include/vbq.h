@@ -250,7 +250,9 @@ vbq_status vbq_qat_workspace_size(int64_t n_groups, size_t* bytes);
  *   logits_dev   float[n_groups][4], 16-byte aligned.
  *   noise_dev    float[n_groups][4] Gumbel noise drawn by the caller, 16-byte
  *                aligned, or NULL for no noise (plain softmax).
- *   tau          temperature, finite and > 0.
+ *   tau          temperature, finite and >= FLT_MIN (the smallest normal
+ *                float); the softmax subtracts the group's largest l + e before
+ *                dividing by tau, so any such tau gives finite pi.
  *   flags        0, or VBQ_QAT_WSOFT_BF16 for a bf16 w_soft; other bits give
  *                VBQ_ERR_UNSUPPORTED.
  *   w_soft_dev   float[n_groups*64] output (bf16[n_groups*64] with
@@ -265,8 +267,8 @@ vbq_status vbq_qat_workspace_size(int64_t n_groups, size_t* bytes);
  * n_groups == 0 does nothing (any pointer may then be NULL; bbar is not
  * written).  Errors: VBQ_ERR_NULL (W, logits or w_soft NULL; workspace NULL
  * with bbar), VBQ_ERR_SHAPE (n_groups out of range),
- * VBQ_ERR_NONFINITE (tau NaN/Inf), VBQ_ERR_UNSUPPORTED (tau <= 0, unknown
- * flags), VBQ_ERR_BUFFER (misaligned pointer or workspace too small),
+ * VBQ_ERR_NONFINITE (tau NaN/Inf), VBQ_ERR_UNSUPPORTED (tau < FLT_MIN,
+ * unknown flags), VBQ_ERR_BUFFER (misaligned pointer or workspace too small),
  * VBQ_ERR_HIP. */
 vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev,
                            const float* logits_dev, const float* noise_dev,
@@ -287,7 +289,7 @@ vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev,
  *   W_dev        float[n_groups*64] the weights of the forward pass.
  *   grad_dev     float[n_groups*64] dL_CE/dw_soft, same layout.
  *   pi_dev       float[n_groups][4] the forward's pi (same tau and noise).
- *   tau          the forward's temperature, finite and > 0.
+ *   tau          the forward's temperature, finite and >= FLT_MIN.
  *   lambda       the bit penalty, finite.
  *   n_bbar       the n that divides bbar (>= 1): this array's n_groups for a
  *                per-matrix penalty, the network's total group count when the
@@ -295,7 +297,7 @@ vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev,
  *   dlogits_dev  float[n_groups][4] output.
  * n_groups == 0 does nothing (pointers may then be NULL).  Errors:
  * VBQ_ERR_SHAPE (n_groups out of range, n_bbar < 1), VBQ_ERR_NONFINITE (tau
- * or lambda NaN/Inf), VBQ_ERR_UNSUPPORTED (tau <= 0), VBQ_ERR_NULL,
+ * or lambda NaN/Inf), VBQ_ERR_UNSUPPORTED (tau < FLT_MIN), VBQ_ERR_NULL,
  * VBQ_ERR_BUFFER (misaligned), VBQ_ERR_HIP. */
 vbq_status vbq_qat_logit_grad(int64_t n_groups, const float* W_dev,
                               const float* grad_dev, const float* pi_dev,

@@ -52,6 +52,7 @@ constexpr int kRowFloats = 68;      // LDS row of one group: 64 weights + 4 floa
 constexpr int kMaxBlocks = 2048;    // one wave per block; eight resident blocks per CU on 256 CUs
 constexpr int kGradBlocks = 2048;   // the gradient's blocks: one tile + a 2 KiB table, eight resident per CU
 constexpr int kBbarThreads = 256;
+constexpr float kMinTau = 1.17549435e-38f;  // the smallest normal float: a subnormal tau may be flushed to 0
 constexpr uint32_t kRsrcFlags = 0x00020000;
 // Cache policy of the bulk weight loads and w_soft stores: non-temporal (each
 // byte is touched once).  Measured on the 131M-class step: 221 us with the
@@ -243,10 +244,12 @@ __global__ __launch_bounds__(64) void vbq_qat_forward_kernel(QatArgs a) {
     const float s1 = sc.s1;
     Cand c2 = sc.c2, c4 = sc.c4, c8 = sc.c8;
 
-    // ---- Gumbel-Softmax weights (section 3.2)
-    const float z0 = (l0 + e0) / a.tau, z1 = (l1 + e1) / a.tau, z2 = (l2 + e2) / a.tau, z3 = (l3 + e3) / a.tau;
-    const float zm = __builtin_fmaxf(__builtin_fmaxf(z0, z1), __builtin_fmaxf(z2, z3));
-    const float p0 = expf(z0 - zm), p1 = expf(z1 - zm), p2 = expf(z2 - zm), p3 = expf(z3 - zm);
+    // ---- Gumbel-Softmax weights (section 3.2); the largest l + e is subtracted
+    // before the division, so a small tau cannot overflow to inf - inf
+    const float v0 = l0 + e0, v1 = l1 + e1, v2 = l2 + e2, v3 = l3 + e3;
+    const float vm = __builtin_fmaxf(__builtin_fmaxf(v0, v1), __builtin_fmaxf(v2, v3));
+    const float p0 = expf((v0 - vm) / a.tau), p1 = expf((v1 - vm) / a.tau), p2 = expf((v2 - vm) / a.tau),
+                p3 = expf((v3 - vm) / a.tau);
     const float psum = (p0 + p1) + (p2 + p3);
     const float pi0 = p0 / psum, pi1 = p1 / psum, pi2 = p2 / psum, pi3 = p3 / psum;
     const float c1 = pi0 * s1;
@@ -506,7 +509,7 @@ vbq_status vbq_qat_forward(int64_t n_groups, const float* W_dev, const float* lo
                            double* bbar_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
   if (n_groups < 0 || n_groups > VBQ_QAT_MAX_GROUPS) return VBQ_ERR_SHAPE;
   if (!(tau == tau) || tau == __builtin_inff() || tau == -__builtin_inff()) return VBQ_ERR_NONFINITE;
-  if (!(tau > 0.0f)) return VBQ_ERR_UNSUPPORTED;
+  if (!(tau >= kMinTau)) return VBQ_ERR_UNSUPPORTED;
   if (flags & ~VBQ_QAT_WSOFT_BF16) return VBQ_ERR_UNSUPPORTED;
   if (n_groups == 0) return VBQ_OK;
   if (!W_dev || !logits_dev || !w_soft_dev) return VBQ_ERR_NULL;
@@ -549,7 +552,7 @@ vbq_status vbq_qat_logit_grad(int64_t n_groups, const float* W_dev, const float*
   if (n_groups < 0 || n_groups > VBQ_QAT_MAX_GROUPS) return VBQ_ERR_SHAPE;
   if (!(tau == tau) || tau == __builtin_inff() || tau == -__builtin_inff()) return VBQ_ERR_NONFINITE;
   if (!(lambda == lambda) || lambda == __builtin_inff() || lambda == -__builtin_inff()) return VBQ_ERR_NONFINITE;
-  if (!(tau > 0.0f)) return VBQ_ERR_UNSUPPORTED;
+  if (!(tau >= kMinTau)) return VBQ_ERR_UNSUPPORTED;
   if (n_bbar < 1) return VBQ_ERR_SHAPE;
   if (n_groups == 0) return VBQ_OK;
   if (!W_dev || !grad_dev || !pi_dev || !dlogits_dev) return VBQ_ERR_NULL;

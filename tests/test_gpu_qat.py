@@ -9,11 +9,13 @@ Bars:
   * pi, w_soft, bbar: the fp32 arithmetic bound below;
   * dL/dlogits of the logit step: the bound derived at _check_grad.
 
-Tolerance (derived from the fp32 arithmetic, u = 2^-24).  With
-z_k = (l_k + e_k)/tau and Z = max_k |z_k| for the group: the sum and the
-division put an error of 2u|z_k| on z_k; the subtraction of the maximum adds
-u(|z_k| + |z_m|); exp contributes at most 2u relative plus the argument's
-absolute error; the normalising sum 3u and the division u.  So every pi_k is
+Tolerance (derived from the fp32 arithmetic, u = 2^-24).  The kernel forms
+v_k = l_k + e_k, subtracts the group's largest v_m and divides by tau.  With
+z_k = v_k/tau and Z = max_k |z_k| for the group: the sums put u|z_k| on each
+z, the subtraction adds u|z_k - z_m| and the division u|z_k - z_m|, so the
+exponent (z_k - z_m) is off by at most 3u(|z_k| + |z_m|); exp contributes at
+most 2u relative plus that absolute error; the normalising sum 3u and the
+division u.  So every pi_k is
 within eps_g = u(12 Z + 8) relative of the exact value; the tests allow
 u(16 Z + 16).  The mix folds pi_k * s_k (one rounding) and adds the four
 terms with FMAs (three roundings), so |w_soft - w*| <= (eps_g + 8u) *
@@ -424,3 +426,19 @@ def test_bf16_one_hot_is_the_rounded_candidate(vbq):
     want = torch.from_numpy(cand.astype(np.float32)).to(torch.bfloat16)  # exact in fp32, then rounded once
     # values compared (a zero candidate of a negative weight may come out as -0.0)
     assert torch.equal(out[0].cpu().reshape(n, 64), want)
+
+
+@pytest.mark.parametrize("tau", [1.17549435e-38, 1e-30])
+def test_tiny_tau_is_one_hot_on_the_noisy_argmax(vbq, tau):
+    # the largest l + e is subtracted before dividing by tau: no inf - inf, pi is exactly
+    # one-hot on argmax(l + e) (every other exponent underflows), as in the oracle
+    n = 4096 + 3
+    W, logits, noise = synth.selection_inputs(n, part=100_000)
+    w_soft, pi, hard, bbar = _run(vbq, W, logits, noise, tau)
+    ref = oqat.forward(W.reshape(n, 64).astype(np.float64), logits.reshape(n, 1, 4), noise.reshape(n, 1, 4), tau)
+    k = np.argmax(logits.astype(np.float32) + noise.astype(np.float32), axis=1)
+    np.testing.assert_array_equal(pi, np.eye(4, dtype=np.float32)[k])
+    np.testing.assert_array_equal(ref["pi"].reshape(n, 4), np.eye(4)[k])
+    cand = oqat.candidates(W.reshape(n, 64).astype(np.float64)).reshape(4, n, 64)
+    assert np.array_equal(w_soft.reshape(n, 64).astype(np.float64), cand[k, np.arange(n)])
+    assert float(bbar[0]) == pytest.approx(WIDTHS[k].mean(), rel=1e-12)

@@ -286,6 +286,8 @@ def test_qat_forward_argument_errors():
     assert f(4, A, A, 0, float("inf"), A, 0, 0, 0, 0, 0, 0) == 5   # tau Inf
     assert f(4, A, A, 0, 0.0, A, 0, 0, 0, 0, 0, 0) == 10           # tau == 0
     assert f(4, A, A, 0, -0.5, A, 0, 0, 0, 0, 0, 0) == 10          # tau < 0
+    assert f(4, A, A, 0, 1e-39, A, 0, 0, 0, 0, 0, 0) == 10         # subnormal tau
+    assert f(0, A, A, 0, 1.2e-38, A, 0, 0, 0, 0, 0, 0) == 0        # the smallest normal tau is accepted
     assert f(4, A + 4, A, 0, 1.0, A, 0, 0, 0, 0, 0, 0) == 7        # W misaligned
     assert f(4, A, A + 8, 0, 1.0, A, 0, 0, 0, 0, 0, 0) == 7        # logits misaligned
     assert f(4, A, A, A + 4, 1.0, A, 0, 0, 0, 0, 0, 0) == 7        # noise misaligned
@@ -309,6 +311,7 @@ def test_qat_logit_grad_argument_errors():
     assert f(4, A, A, A, float("nan"), 0.5, 4, A, 0) == 5          # tau NaN
     assert f(4, A, A, A, 1.0, float("inf"), 4, A, 0) == 5          # lambda Inf
     assert f(4, A, A, A, -1.0, 0.5, 4, A, 0) == 10                 # tau < 0
+    assert f(4, A, A, A, 1e-39, 0.5, 4, A, 0) == 10                # subnormal tau
     assert f(4, 0, A, A, 1.0, 0.5, 4, A, 0) == 1                   # W NULL
     assert f(4, A, 0, A, 1.0, 0.5, 4, A, 0) == 1                   # grad NULL
     assert f(4, A, A, 0, 1.0, 0.5, 4, A, 0) == 1                   # pi NULL
