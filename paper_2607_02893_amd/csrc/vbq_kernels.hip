@@ -964,6 +964,14 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
 // Both read the unit's class runs from the unit table (rows u and u + 1), so
 // both issue their first code loads at once.  Workgroup barriers separate
 // the set-up, the decode and the row reduction.
+//
+// The roles do unequal VALU work (the 1-bit run is most of the entries), and
+// a workgroup's waves are dealt to the CU's four SIMDs in turn, so with pairs
+// (2k, 2k + 1) a CU holding one workgroup puts every role-0 wave on two SIMDs
+// and every role-1 wave on the other two (measured with the hardware ids of
+// each wave).  When more than half of the pairs have a unit, pair k is waves
+// k and k + NW/2 instead: both land on one SIMD, so every SIMD carries both
+// roles.  With fewer units, (2k, 2k + 1) spreads the busy waves over more SIMDs.
 // ---------------------------------------------------------------------------
 template <int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) void vbq_mv_pair_kernel(
@@ -988,7 +996,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
   const uint32_t lane = lane_id();
   const int wave = wave_id();
-  const int pair = wave >> 1, role = wave & 1;
+  const bool mix = U > NP / 2;  // wave-uniform
+  const int pair = mix ? wave % NP : wave >> 1, role = mix ? wave / NP : wave & 1;
   const int t = blockIdx.x;
   const WavePlan P = wave_plan(R, SW, 1);
   const uint32_t ysum = lds0 + (uint32_t)(pair * R * 4);
