@@ -242,6 +242,10 @@ __device__ __forceinline__ uint32_t opaque(uint32_t v) {
   __asm__ __volatile__("" : "+s"(v));
   return v;
 }
+__device__ __forceinline__ uint64_t opaque64(uint64_t v) {
+  __asm__ __volatile__("" : "+s"(v));
+  return v;
+}
 
 // ---------------------------------------------------------------------------
 // Work split.  A workgroup of NW waves owns one row tile.  Each unit of the
@@ -792,7 +796,9 @@ __device__ __forceinline__ int clamp_run(const DevMatrix& mat, int c, uint32_t s
 // UNI >= 0: every group of the matrix has width class UNI (a uniform "recipe"
 // matrix, one row only).  Entries then sit at consecutive real positions, so
 // the width map, the class counts and the index are not needed, and a unit's
-// first entry follows from the geometry.
+// first entry follows from the geometry.  The three width-map arguments then
+// carry the class's code offset, scale offset and entry count instead, which
+// the first code loads need.
 template <int MT, int NW, int UNI = -1>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 4 : 2))) void vbq_mv_kernel(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ blob, uint32_t off_wmap, uint32_t tile_words,
@@ -801,9 +807,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   DevMatrix mat = a.m;
   mat.blob = blob;
-  mat.off_wmap = off_wmap;
-  mat.tile_words = tile_words;
-  mat.chunk_words = chunk_words;
+  if constexpr (UNI >= 0) {
+    // no width map: these three carry the one class's code and scale offsets
+    // and entry count, which the first code loads need
+    mat.off_codes[UNI] = off_wmap;
+    mat.off_scales[UNI] = tile_words;
+    mat.n_entries[UNI] = chunk_words;
+  } else {
+    mat.off_wmap = off_wmap;
+    mat.tile_words = tile_words;
+    mat.chunk_words = chunk_words;
+  }
   mat.wmap_words = wmap_words;
   mat.G = G;
   mat.N = N;
@@ -1157,9 +1171,9 @@ struct MmBlock {
 // codes start at byte (2h << c) & ~3 of the entry.  Loads are unconditional
 // (clamped), so several blocks stay in flight.
 template <int RB>
-__device__ __forceinline__ void load_mm_block(MmBlock& bk, const MmArgs& a, const DevMatrix& mat, uint32_t fwd,
-                                              int f, int rg, int rows, const MmClassInfo& ci, int j0,
-                                              uint32_t lane) {
+__device__ __forceinline__ void load_mm_block(MmBlock& bk, const uint16_t* xp, int64_t ldx, int M,
+                                              const DevMatrix& mat, uint32_t fwd, int f, int rg, int rows,
+                                              const MmClassInfo& ci, int j0, uint32_t lane) {
   const int R = mat.R;
   const uint32_t e = lane & 15u, h = lane >> 4;
   const int col = f / RB;
@@ -1172,8 +1186,8 @@ __device__ __forceinline__ void load_mm_block(MmBlock& bk, const MmArgs& a, cons
   bk.w = ld<u32x4>(mat.blob, sel4(ci.offc, c) + (g << (3 + c)) + (((2u * h) << c) & ~3u));
   const uint16_t sb = ld<uint16_t>(mat.blob, sel4(ci.offs, c) + 2u * g);
   bk.s = real ? sb : (uint16_t)0;
-  const int m = min((int)e, a.M - 1);
-  const u32x4* xr = (const u32x4*)(a.x + (size_t)m * a.ldx + (size_t)(j0 + col) * 64 + 16 * h);
+  const int m = min((int)e, M - 1);
+  const u32x4* xr = (const u32x4*)(xp + (size_t)m * ldx + (size_t)(j0 + col) * 64 + 16 * h);
   bk.a0 = xr[0];
   bk.a1 = xr[1];
 }
@@ -1216,11 +1230,28 @@ __device__ __forceinline__ void mm_done(const MmBlock& bk) {
   __asm__ __volatile__("" ::"v"(bk.w), "v"(bk.s), "v"(bk.a0), "v"(bk.a1), "v"(bk.c));
 }
 
+// As for the one-row kernel, the values the first loads depend on come as
+// preloaded leading arguments (geo packs R, C, log2 R and S the same way),
+// the unit table is read beside the width map rather than after it, and the
+// argument block is read only once those loads are issued.
 template <int NW, int RB>
-__global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(MmArgs a) {
+__global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(const uint8_t* __restrict__ blob, uint32_t off_wmap,
+                                                         uint32_t tile_words, uint32_t chunk_words, uint32_t wmap_words,
+                                                         int32_t G, int32_t N, uint32_t geo, int32_t U, MmArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  const DevMatrix& mat = a.m;
-  const int R = mat.R, S = a.S;
+  DevMatrix mat = a.m;
+  mat.blob = blob;
+  mat.off_wmap = off_wmap;
+  mat.tile_words = tile_words;
+  mat.chunk_words = chunk_words;
+  mat.wmap_words = wmap_words;
+  mat.G = G;
+  mat.N = N;
+  mat.U = U;
+  mat.R = (int)(geo & 0x1FF);
+  mat.C = (int)((geo >> 9) & 0xFF);
+  mat.logR = (int)((geo >> 17) & 0xF);
+  const int R = mat.R, S = (int)(geo >> 21);
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
   const int wave = wave_id();
   const int t = blockIdx.x;  // one row tile per workgroup
@@ -1244,14 +1275,22 @@ __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(MmArgs a) {
     if (cb >= ce) continue;  // wave-uniform: an empty slice
     const int wb = (cb * R) >> 6, we = (ce * R + 63) >> 6;
     const WmapRegs wr = load_wmap(mat, u, we, lane);
+    const u32x16 rows2 = unit_rows(mat, unit);  // beside the width map, not after it
+    const uint32_t es[4] = {rows2.s0, rows2.s1, rows2.s2, rows2.s3};
+    // values from the kernel-argument block only after the loads above are
+    // issued (the compiler would otherwise hoist them and wait for the block)
+    lds_phase();
+    const uint16_t* xp = (const uint16_t*)opaque64((uint64_t)a.x);
+    const int64_t ldx = (int64_t)opaque64((uint64_t)a.ldx);
+    const int M = (int)opaque((uint32_t)a.M);
     const WinCounts wc = window_counts(wr, u, wb, we, R, lane);
     MmClassInfo ci;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      ci.start[c] = uniform((int)(class_start(mat, unit, c) + wc.before[c]));
-      ci.lim[c] = uniform((int)(max(mat.n_entries[c], 1u) - 1u));
-      ci.offc[c] = uniform((int)mat.off_codes[c]);
-      ci.offs[c] = uniform((int)mat.off_scales[c]);
+      ci.start[c] = uniform((int)(es[c] + wc.before[c]));
+      ci.lim[c] = uniform((int)(max(opaque(mat.n_entries[c]), 1u) - 1u));
+      ci.offc[c] = opaque(mat.off_codes[c]);
+      ci.offs[c] = opaque(mat.off_scales[c]);
     }
     build_index<true>(wr, u, wb, we, R, wc, fwd, lane);
     lds_phase();
@@ -1263,21 +1302,21 @@ __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(MmArgs a) {
 #pragma unroll
       for (int i = 0; i < RB; ++i) acc[i] = float4_t{0.0f, 0.0f, 0.0f, 0.0f};
       MmBlock B0, B1, B2, B3;
-      load_mm_block<RB>(B0, a, mat, fwd, 0, rg, rows, ci, j0, lane);
-      load_mm_block<RB>(B1, a, mat, fwd, min(1, last), rg, rows, ci, j0, lane);
-      load_mm_block<RB>(B2, a, mat, fwd, min(2, last), rg, rows, ci, j0, lane);
+      load_mm_block<RB>(B0, xp, ldx, M, mat, fwd, 0, rg, rows, ci, j0, lane);
+      load_mm_block<RB>(B1, xp, ldx, M, mat, fwd, min(1, last), rg, rows, ci, j0, lane);
+      load_mm_block<RB>(B2, xp, ldx, M, mat, fwd, min(2, last), rg, rows, ci, j0, lane);
       // four blocks in flight; block f adds into acc[f % RB] (the ring slot)
       for (int f = 0; f < nf; f += 4) {
-        load_mm_block<RB>(B3, a, mat, fwd, min(f + 3, last), rg, rows, ci, j0, lane);
+        load_mm_block<RB>(B3, xp, ldx, M, mat, fwd, min(f + 3, last), rg, rows, ci, j0, lane);
         acc[0 % RB] += mm_products(B0, h);
         mm_done(B0);
-        load_mm_block<RB>(B0, a, mat, fwd, min(f + 4, last), rg, rows, ci, j0, lane);
+        load_mm_block<RB>(B0, xp, ldx, M, mat, fwd, min(f + 4, last), rg, rows, ci, j0, lane);
         if (f + 1 < nf) acc[1 % RB] += mm_products(B1, h);
         mm_done(B1);
-        load_mm_block<RB>(B1, a, mat, fwd, min(f + 5, last), rg, rows, ci, j0, lane);
+        load_mm_block<RB>(B1, xp, ldx, M, mat, fwd, min(f + 5, last), rg, rows, ci, j0, lane);
         if (f + 2 < nf) acc[2 % RB] += mm_products(B2, h);
         mm_done(B2);
-        load_mm_block<RB>(B2, a, mat, fwd, min(f + 6, last), rg, rows, ci, j0, lane);
+        load_mm_block<RB>(B2, xp, ldx, M, mat, fwd, min(f + 6, last), rg, rows, ci, j0, lane);
         if (f + 3 < nf) acc[3 % RB] += mm_products(B3, h);
         mm_done(B3);
       }
@@ -1291,7 +1330,7 @@ __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(MmArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int m = 4 * (int)h + j;
-          if (m < a.M && row < rows) {
+          if (m < M && row < rows) {
             const uint32_t ya = ysum + 4u * (uint32_t)(m * R + row);
             lds_store_f32(ya, lds_f32(ya) + acc[i][j]);
           }
@@ -1485,6 +1524,11 @@ vbq_status launch_mv_nw(const MvArgs& a, int lds, hipStream_t s) {
   const uint16_t* x = a.x;
   const uint8_t* blob = a.m.blob;
   uint32_t off_wmap = a.m.off_wmap, tile_words = a.m.tile_words, chunk_words = a.m.chunk_words;
+  if constexpr (UNI >= 0) {  // (the kernel reads them as such)
+    off_wmap = a.m.off_codes[UNI];
+    tile_words = a.m.off_scales[UNI];
+    chunk_words = a.m.n_entries[UNI];
+  }
   uint32_t wmap_words = a.m.wmap_words;
   int32_t G = a.m.G, N = a.m.N, U = a.m.U;
   uint32_t geo = (uint32_t)a.m.R | ((uint32_t)a.m.C << 9) | ((uint32_t)a.m.logR << 17) | ((uint32_t)a.S << 21);
@@ -1613,7 +1657,12 @@ vbq_status launch_mm_nw(const MmArgs& a, int lds, hipStream_t s) {
     if (st != VBQ_OK) return st;
   }
   MmArgs args = a;
-  void* kargs[] = {&args};
+  const uint8_t* blob = a.m.blob;
+  uint32_t off_wmap = a.m.off_wmap, tile_words = a.m.tile_words, chunk_words = a.m.chunk_words;
+  uint32_t wmap_words = a.m.wmap_words;
+  int32_t G = a.m.G, N = a.m.N, U = a.m.U;
+  uint32_t geo = (uint32_t)a.m.R | ((uint32_t)a.m.C << 9) | ((uint32_t)a.m.logR << 17) | ((uint32_t)a.S << 21);
+  void* kargs[] = {&blob, &off_wmap, &tile_words, &chunk_words, &wmap_words, &G, &N, &geo, &U, &args};
   return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
 }
 
