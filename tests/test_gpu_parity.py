@@ -71,9 +71,12 @@ def test_gemv_matches_oracle(vbq, N, K, R, C):
 
 
 # geometries the two-waves-per-unit kernel takes (mixed widths, 2..8 units
-# of at most 32 columns per tile, a small grid), with ragged tiles and units
+# of at most 32 columns per tile, a small grid), with ragged tiles and units;
+# units per tile 2 (pairs of adjacent waves), 3-4 (eight waves) and 5-8
+# (sixteen waves), so both ways of pairing waves, with and without idle pairs
 PAIR_GEOMS = [(6144, 4096, 0, 0), (4096, 14336, 0, 0), (1000, 4096, 0, 0), (37, 320, 0, 0), (17, 896, 0, 0),
-              (300, 640, 256, 3), (130, 1024, 32, 5), (77, 2048, 64, 11)]
+              (300, 640, 256, 3), (130, 1024, 32, 5), (77, 2048, 64, 11), (200, 2048, 16, 16),
+              (150, 640, 16, 2), (90, 768, 32, 2), (50, 448, 16, 1)]
 
 
 @pytest.mark.parametrize("N,K,R,C", PAIR_GEOMS)
