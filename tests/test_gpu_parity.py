@@ -287,7 +287,7 @@ def test_workload_matrices_full_size(vbq, cfg):
     mats = wl.matrices if cfg == 0 else [m for m in wl.matrices if m.layer in (0, 1) and m.proj in (0, 3)] + \
         [m for m in wl.matrices if m.layer == 0 and m.proj in (1, 2)] + [wl.matrices[-1]]
     for spec in mats:
-        for M in ((1, 16) if cfg == 4 else (1,)):
+        for M in ((1, 2, 4, 8, 16) if cfg == 4 else (1,)):  # every batch size bench.py times
             w = _sampled_check(vbq, spec, wl.seed, M=M)
             _say(f"cfg{cfg} {spec.name} L{spec.layer} {spec.N}x{spec.K} M={M}: max rel err {w:.2e}")
 
