@@ -324,6 +324,31 @@ def test_gemv_rows_index_map(vbq):
     assert np.all(y[untouched] == -7.0)
 
 
+def test_gemv_rows_repeated_indices_and_empty_output(vbq):
+    """Rows sharing an index write one of their own values there (which one is
+    not defined); with y_len = 0 every index is outside y and nothing is
+    written."""
+    spec = synth.MatrixSpec("t", 0, 0, 300, 640)
+    bits, q, s = synth.make_matrix(spec, 83)
+    Wp = _packed(vbq, q, s, bits)
+    xd = _x_dev(synth.make_x(spec, 83)[0])
+    y_ref = Wp.gemv(xd).cpu().numpy()
+    ylen = 40
+    rows = (np.arange(spec.N) % ylen).astype(np.int32)  # every index shared by 7 or 8 rows
+    y = torch.full((ylen,), -7.0, dtype=torch.float32, device="cuda")
+    Wp.gemv_rows(xd, y, torch.from_numpy(rows).cuda())
+    y = y.cpu().numpy()
+    for i in range(ylen):
+        assert y[i] in set(y_ref[rows == i].tolist()), i
+    y0 = torch.full((8,), -7.0, dtype=torch.float32, device="cuda")
+    rows_d = torch.from_numpy(rows).cuda()
+    st = vbq.raw_gemv_rows(Wp.desc, Wp.blob.data_ptr(), xd.data_ptr(), y0.data_ptr(), 0, rows_d.data_ptr(),
+                           torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    torch.cuda.synchronize()
+    assert np.all(y0.cpu().numpy() == -7.0)
+
+
 @pytest.mark.parametrize("N,K", [(3000, 1024), (700, 4096), (100, 640)])
 def test_row_buckets_match_oracle(vbq, N, K):
     """A frequency-tiered head (the recipe's 8/4/2/1-bit rows) packed as four
