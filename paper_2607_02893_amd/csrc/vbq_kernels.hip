@@ -968,7 +968,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
 }
 
 // ---------------------------------------------------------------------------
-// Two waves per unit (one activation row, mixed widths, small matrices).
+// Two waves per unit (one or two activation rows, mixed widths, small matrices).
 //
 // With one wave per unit a small matrix leaves each SIMD one or two waves,
 // and every wave runs its index build and its four class runs one after the
@@ -986,9 +986,14 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
 // each wave).  When more than half of the pairs have a unit, pair k is waves
 // k and k + NW/2 instead: both land on one SIMD, so every SIMD carries both
 // roles.  With fewer units, (2k, 2k + 1) spreads the busy waves over more SIMDs.
+//
+// MT = 2 activation rows uses the same split (x of both rows staged straight
+// from memory by role 1, the 8-bit batch loaded when its turn comes), in
+// 8-wave workgroups only: two rows need more than the 128 registers a wave of
+// a 16-wave workgroup can have.
 // ---------------------------------------------------------------------------
-template <int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) void vbq_mv_pair_kernel(
+template <int NW, int MT>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 4 : 2))) void vbq_mv_pair_kernel(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ blob, uint32_t off_wmap, uint32_t tile_words,
     uint32_t chunk_words, uint32_t wmap_words, int32_t G, int32_t N, uint32_t geo, int32_t U, uint32_t sw_m,
     MvArgs a) {
@@ -1006,6 +1011,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
   mat.R = (int)(geo & 0x1FF);
   mat.C = (int)((geo >> 9) & 0xFF);
   mat.logR = (int)((geo >> 17) & 0xF);
+  a.x = x;
+  a.M = (int)(sw_m >> 16);
   const int R = mat.R, SW = (int)(sw_m & 0xFFFF);
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
   const uint32_t lane = lane_id();
@@ -1013,9 +1020,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
   const bool mix = U > NP / 2;  // wave-uniform
   const int pair = mix ? wave % NP : wave >> 1, role = mix ? wave / NP : wave & 1;
   const int t = blockIdx.x;
-  const WavePlan P = wave_plan(R, SW, 1);
-  const uint32_t ysum = lds0 + (uint32_t)(pair * R * 4);
-  const uint32_t region = lds0 + (uint32_t)(NP * R * 4 + pair * P.bytes);
+  const WavePlan P = wave_plan(R, SW, MT);
+  const uint32_t ysum = lds0 + (uint32_t)(pair * MT * R * 4);
+  const uint32_t region = lds0 + (uint32_t)(NP * MT * R * 4 + pair * P.bytes);
   Win wn;
   wn.xs = region + P.xs;
   wn.Xs = region + P.Xs;
@@ -1026,15 +1033,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
   wn.logR = mat.logR;
   const uint32_t inv = region + P.inv;
   if (role == 0)
-    for (int i = (int)lane; i < R; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
+    for (int i = (int)lane; i < MT * R; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
 
   const bool active = pair < mat.U;  // wave-uniform
   const UnitInfo u = load_unit(mat, t, active ? pair : 0);
   const int unit = t * mat.U + (active ? pair : 0);
-  Batch<0, 1> A0;
-  Batch<1, 1> A1;
-  Batch<2, 1> A2;
-  Batch<3, 1> A3;
+  Batch<0, MT> A0;
+  Batch<1, MT> A1;
+  Batch<2, MT> A2;
+  Batch<3, MT> A3;
   uint32_t start[4], seg[4];
   int n[4];
   if (active) {
@@ -1042,7 +1049,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
     XRegs xr;
     if (role == 0)
       wr = load_wmap(mat, u, u.W, lane);
-    else
+    else if constexpr (MT == 1)
       load_x1(x, u.j0, u.cols, xr, lane);
     const u32x16 rows2 = unit_rows(mat, unit);
     const u32x4 erow = rows2.s0123, own = rows2.s89ab - rows2.s0123;
@@ -1071,34 +1078,46 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
       o += wc.own[c];
     }
     if (role == 0) {
-      load_batch<0, 1>(A0, mat, start[0], n[0], 0, lane);
+      load_batch<0, MT>(A0, mat, start[0], n[0], 0, lane);
       build_index(wr, u, 0, u.W, R, wc, inv, lane);
     } else {
-      load_batch<1, 1>(A1, mat, start[1], n[1], 0, lane);
-      load_batch<2, 1>(A2, mat, start[2], n[2], 0, lane);
-      load_batch<3, 1>(A3, mat, start[3], n[3], 0, lane);
-      store_x1(u.cols, xr, wn, lane);
+      load_batch<1, MT>(A1, mat, start[1], n[1], 0, lane);
+      load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
+      if constexpr (MT == 1) {
+        load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
+        store_x1(u.cols, xr, wn, lane);
+      } else {
+        stage_x<MT>(a, u.j0, u.cols, wn, lane);  // (several rows: straight from memory to LDS)
+      }
     }
   }
   __syncthreads();  // the index and x of every unit are in LDS
   if (active) {
     if (role == 0) {
-      run_class<0, 1>(mat, A0, start[0], n[0], seg[0], wn, lane);
+      run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
     } else {
-      run_class<1, 1>(mat, A1, start[1], n[1], seg[1], wn, lane);
-      run_class<2, 1>(mat, A2, start[2], n[2], seg[2], wn, lane);
-      run_class<3, 1>(mat, A3, start[3], n[3], seg[3], wn, lane);
+      run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
+      run_class<2, MT>(mat, A2, start[2], n[2], seg[2], wn, lane);
+      // several rows need the registers: the 8-bit batch is loaded when its turn comes
+      if constexpr (MT > 1) load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
+      run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
     }
   }
   __syncthreads();  // every partial product is in LDS
-  if (active && role == 0) reduce_window<1>(wn, R, u.cols, u.rows, ysum, lane);
+  if (active && role == 0) reduce_window<MT>(wn, R, u.cols, u.rows, ysum, lane);
   __syncthreads();
   const int rows = min(R, mat.N - t * R);
-  for (int r = threadIdx.x; r < rows; r += NW * 64) {
-    float tot = 0.0f;
+  for (int slot = threadIdx.x; slot < MT * R; slot += NW * 64) {
+    const int m = slot >> mat.logR, r = slot & (R - 1);
+    if (m < a.M && r < rows) {
+      float tot = 0.0f;
 #pragma unroll
-    for (int p2 = 0; p2 < NP; ++p2) tot += lds_f32(lds0 + 4u * (uint32_t)(p2 * R + r));
-    store_row(a, (size_t)t * R + r, tot);
+      for (int p2 = 0; p2 < NP; ++p2) tot += lds_f32(lds0 + 4u * (uint32_t)(p2 * MT * R + slot));
+      if constexpr (MT == 1)
+        store_row(a, (size_t)t * R + r, tot);
+      else
+        a.y[m * a.ldy + (size_t)t * R + r] = tot;
+    }
   }
 }
 
@@ -1542,9 +1561,9 @@ vbq_status launch_mv_nw(const MvArgs& a, int lds, hipStream_t s) {
 // leave the SIMDs with at most two waves each.
 constexpr int kPairMaxUnits = 2048;
 
-template <int NW>
+template <int NW, int MT>
 vbq_status launch_pair_nw(const MvArgs& a, int lds, hipStream_t s) {
-  const void* kernel = (const void*)vbq_mv_pair_kernel<NW>;
+  const void* kernel = (const void*)vbq_mv_pair_kernel<NW, MT>;
   if (lds > 64 * 1024) {
     static std::atomic<uint64_t> done{0};
     vbq_status st = allow_big_lds(kernel, done);
@@ -1557,47 +1576,54 @@ vbq_status launch_pair_nw(const MvArgs& a, int lds, hipStream_t s) {
   uint32_t wmap_words = a.m.wmap_words;
   int32_t G = a.m.G, N = a.m.N, U = a.m.U;
   uint32_t geo = (uint32_t)a.m.R | ((uint32_t)a.m.C << 9) | ((uint32_t)a.m.logR << 17) | (1u << 21);
-  uint32_t sw_m = (uint32_t)a.SW | (1u << 16);
+  uint32_t sw_m = (uint32_t)a.SW | ((uint32_t)a.M << 16);
   void* kargs[] = {&x, &blob, &off_wmap, &tile_words, &chunk_words, &wmap_words, &G, &N, &geo, &U, &sw_m, &args};
   return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
 }
 
-// Launches the pair kernel when the matrix qualifies; *used says whether it did.
-vbq_status try_launch_pair(const DevMatrix& m, const void* x, float* y, const int32_t* rows, int64_t ylen, hipStream_t s,
-                           bool* used) {
+// Launches the pair kernel for MT (1 or 2) activation rows when the matrix
+// qualifies; *used says whether it did.
+template <int MT>
+vbq_status try_launch_pair(const DevMatrix& m, const void* x, int64_t ldx, float* y, int64_t ldy, const int32_t* rows,
+                           int64_t ylen, hipStream_t s, bool* used) {
   *used = false;
   int classes = 0;
   for (int c = 0; c < 4; ++c) classes += m.n_entries[c] ? 1 : 0;
   if (classes < 2 || m.U < 2 || m.U > 8 || m.C > kXRegs * 8) return VBQ_OK;
-  if ((int64_t)m.T * m.U > kPairMaxUnits) return VBQ_OK;
+  // (two rows: a grid half as large, beyond which the one-wave kernel is faster)
+  if ((int64_t)m.T * m.U > (MT == 1 ? kPairMaxUnits : kPairMaxUnits / 2)) return VBQ_OK;
+  // two rows fit the registers of 8 waves per workgroup (2 per SIMD), not of 16
+  if (MT > 1 && m.U > 4) return VBQ_OK;
   const int NW = m.U <= 4 ? 8 : 16;
-  const int lds = (NW / 2) * (m.R * 4 + wave_plan(m.R, m.C, 1).bytes);
+  const int lds = (NW / 2) * (MT * m.R * 4 + wave_plan(m.R, m.C, MT).bytes);
   if (lds > kLdsLimit) return VBQ_OK;
   MvArgs a;
   a.m = m;
   a.x = (const uint16_t*)x;
   a.y = y;
-  a.ldx = m.K;
-  a.ldy = m.N;
-  a.M = 1;
+  a.ldx = ldx;
+  a.ldy = ldy;
+  a.M = MT;
   a.S = 1;
   a.SW = m.C;
-  a.rows = rows;
+  a.rows = MT == 1 ? rows : nullptr;
   a.ylen = ylen;
   *used = true;
-  return NW == 8 ? launch_pair_nw<8>(a, lds, s) : launch_pair_nw<16>(a, lds, s);
+  if constexpr (MT == 1)
+    if (NW == 16) return launch_pair_nw<16, 1>(a, lds, s);
+  return launch_pair_nw<8, MT>(a, lds, s);
 }
 
 template <int MT>
 vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, float* y, int64_t ldy, hipStream_t s,
                      const int32_t* rows = nullptr, int64_t ylen = 0) {
-  if constexpr (MT == 1) {
+  if constexpr (MT <= 2) {
     // VBQ_ONE_WAVE_PER_UNIT=1 turns the pair kernel off (to test both paths
     // on the same inputs)
     const char* one = getenv("VBQ_ONE_WAVE_PER_UNIT");
     if (!(one && one[0] == '1')) {
       bool used = false;
-      const vbq_status st = try_launch_pair(m, x, y, rows, ylen, s, &used);
+      const vbq_status st = try_launch_pair<MT>(m, x, ldx, y, ldy, rows, ylen, s, &used);
       if (used) return st;
     }
   }

@@ -100,6 +100,18 @@ def test_pair_kernel_matches_one_wave_per_unit(vbq, N, K, R, C, monkeypatch):
     want, mag = omatmul.gemv(q, s, x), omatmul.row_magnitude(q, s, x)
     parity.check(y_pair, want, mag, what=f"pair gemv {N}x{K}")
     parity.check(y_one, want, mag, what=f"one-wave gemv {N}x{K}")
+    # two activation rows (the pair kernel takes up to four units per tile)
+    X = synth.make_x(spec, 47, M=2)
+    Xd = torch.from_numpy(np.ascontiguousarray(X)).to("cuda")
+    Y_pair = Wp.gemm_small(Xd).cpu().numpy()
+    monkeypatch.setenv("VBQ_ONE_WAVE_PER_UNIT", "1")
+    Y_one = Wp.gemm_small(Xd).cpu().numpy()
+    monkeypatch.delenv("VBQ_ONE_WAVE_PER_UNIT")
+    if Wp.desc.n_chunks >= 4:
+        assert np.array_equal(Y_pair, Y_one)
+    for m in range(2):
+        parity.check(Y_pair[m], omatmul.gemv(q, s, X[m]), omatmul.row_magnitude(q, s, X[m]),
+                     what=f"pair gemm_small {N}x{K} m={m}")
 
 
 def test_one_hot_probe_is_exact(vbq):
