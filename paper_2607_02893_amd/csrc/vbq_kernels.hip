@@ -973,8 +973,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
 // With one wave per unit a small matrix leaves each SIMD one or two waves,
 // and every wave runs its index build and its four class runs one after the
 // other, each a chain of LDS round trips.  Here a pair of waves shares the
-// unit: wave 2k loads the width map, builds the index and decodes the 1-bit
-// run; wave 2k + 1 loads x, stages it and decodes the 2-, 4- and 8-bit runs.
+// unit: role 0 loads the width map, builds the index and decodes the 1-bit
+// run; role 1 loads x, stages it and decodes the 2-, 4- and 8-bit runs.
 // Both read the unit's class runs from the unit table (rows u and u + 1), so
 // both issue their first code loads at once.  Workgroup barriers separate
 // the set-up, the decode and the row reduction.
@@ -1556,9 +1556,10 @@ vbq_status launch_mv_nw(const MvArgs& a, int lds, hipStream_t s) {
   return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
 }
 
-// Wave pairs: one row, mixed widths, whole units of at most 32 columns, at
-// most 8 units per tile, and a grid small enough that one wave per unit would
-// leave the SIMDs with at most two waves each.
+// Wave pairs: one or two rows, mixed widths, whole units of at most 32
+// columns, at most 8 units per tile (4 for two rows), and a grid small enough
+// that one wave per unit would leave the SIMDs with at most two waves each
+// (half as large for two rows).
 constexpr int kPairMaxUnits = 2048;
 
 template <int NW, int MT>
