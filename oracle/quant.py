@@ -14,7 +14,9 @@ Readings (the paper is silent on these):
   * sign(w) is +1 for w >= 0, including -0.0, so that a 1-bit group is a pure
     +/-1 code;
   * the 1-bit mean is the sequential double-precision sum of |w_i| over
-    i = 0..63, divided by 64.
+    i = 0..63, divided by 64;
+  * a scale whose fp16 rounding is infinite (max|w| / qmax, or the 1-bit mean,
+    at or beyond 65520) is an error at every width: OverflowError.
 """
 
 import numpy as np
@@ -71,6 +73,8 @@ def quantize_group(w, b, group=G, exact_scale=False):
             total += abs(v)
         s_exact = total / group
         s_out = s_exact if exact_scale else fp16_bits(s_exact)
+        if not exact_scale and not np.isfinite(fp16_value(s_out)):
+            raise OverflowError("scale overflows fp16")  # the stored scale must be a finite fp16 value
         return [one_bit_sign(v) for v in w], s_out
     m = qmax(b)
     amax = 0.0
@@ -121,7 +125,10 @@ def quantize(W, bits):
             total = np.zeros(wg.shape[0], dtype=np.float64)
             for i in range(G):  # sequential double sum, i = 0..63
                 total = total + np.abs(wg[:, i])
-            s16[sel] = (total / G).astype(np.float16)
+            s = (total / G).astype(np.float16)
+            if not np.all(np.isfinite(s)):
+                raise OverflowError("scale overflows fp16")
+            s16[sel] = s
             q[sel] = np.where(wg >= 0.0, 1, -1)
         else:
             m = qmax(b)

@@ -160,6 +160,17 @@ def test_error_paths():
     W[1, 3] = 1e6  # max|w|/1 overflows fp16
     assert _status(lambda: vbq.pack(W, b4)) == "VBQ_ERR_SCALE_RANGE"
     W[1, 3] = 0.0
+    # 1 bit: a mean |w| at or beyond 65520 rounds to +inf, like the oracle's OverflowError
+    b1 = np.ones((4, 2), dtype=np.uint8)
+    W1 = np.zeros((4, 128), dtype=np.float32)
+    W1[2, :64] = 1e6
+    assert _status(lambda: vbq.pack(W1, b1)) == "VBQ_ERR_SCALE_RANGE"
+    W1[2, :64] = -65520.0
+    assert _status(lambda: vbq.pack(W1, b1)) == "VBQ_ERR_SCALE_RANGE"
+    W1[2, :64] = 65519.99  # rounds to 65504, the largest fp16: packs
+    blob1, d1 = vbq.pack(W1, b1)
+    q1, s1, _ = olayout.unpack(np.asarray(blob1), d1.info())
+    assert int(s1[2, 0]) == 0x7BFF
     assert _status(lambda: vbq.pack(W, b4, tile_rows=24)) == "VBQ_ERR_UNSUPPORTED"
     assert _status(lambda: vbq.pack(W, b4, tile_rows=64, chunk_groups=200)) == "VBQ_ERR_UNSUPPORTED"
     assert _status(lambda: vbq.pack_size(np.ones((4, 2), np.uint8), 100)) == "VBQ_ERR_SHAPE"

@@ -173,10 +173,24 @@ def test_zero_group_and_negative_zero():
 
 @pytest.mark.filterwarnings("ignore:overflow encountered in cast")
 def test_scale_overflow_raises():
+    """A stored scale must be a finite fp16 value at every width (reading R3);
+    the packer reports the same groups as VBQ_ERR_SCALE_RANGE."""
     with pytest.raises(OverflowError):
         quant.quantize_group([1e6] + [0.0] * 63, 2)
     with pytest.raises(OverflowError):
         quant.quantize(np.array([[1e6] + [0.0] * 63]), np.array([[4]]))
+    # 1 bit: the mean |w| is the scale; 1e6 rounds to +inf in fp16
+    with pytest.raises(OverflowError):
+        quant.quantize_group([1e6] * 64, 1)
+    with pytest.raises(OverflowError):
+        quant.quantize(np.array([[1e6] * 64]), np.array([[1]]))
+    # 65519.99 rounds down to 65504 (the largest fp16), 65520 rounds to +inf
+    q, sb = quant.quantize_group([65519.99] * 64, 1)
+    assert sb == 0x7BFF and q == [1] * 64
+    with pytest.raises(OverflowError):
+        quant.quantize_group([-65520.0] * 64, 1)
+    qv, sv = quant.quantize(np.array([[65519.99] * 64]), np.array([[1]]))
+    assert int(sv[0, 0]) == 0x7BFF
 
 
 def test_group_size_one_is_degenerate():
@@ -408,6 +422,25 @@ def test_pins_catch_planted_mistakes(golden_dir, monkeypatch, mutation):
         monkeypatch.setattr(quant, "fp16_bits", record)
     with pytest.raises(AssertionError):
         test_hand_computed_groups(golden_dir)
+
+
+def test_pins_catch_unchecked_one_bit_overflow(monkeypatch):
+    """Plant the mistake of returning the fp16 bits of +inf for a 1-bit group
+    whose mean |w| overflows (the b >= 2 check alone): the overflow pin fails."""
+    orig = quant.quantize_group
+
+    def unchecked(w, b, **kw):
+        if b == 1:
+            total = 0.0
+            for v in w:
+                total += abs(float(v))
+            return [quant.one_bit_sign(float(v)) for v in w], quant.fp16_bits(total / 64)
+        return orig(w, b, **kw)
+    monkeypatch.setattr(quant, "quantize_group", unchecked)
+    with pytest.raises(BaseException) as err:
+        with np.errstate(over="ignore"):
+            test_scale_overflow_raises()
+    assert "DID NOT RAISE" in str(err.value)
 
 
 _last_exact = [0.0]

@@ -199,6 +199,22 @@ def test_logit_grad_matches_central_differences():
     np.testing.assert_allclose(d.sum(axis=-1), 0.0, atol=1e-12)
 
 
+def test_logit_grad_without_cross_entropy_is_the_penalty_gradient():
+    """With G = 0 (the reading of section 3.3 (i) in which cross-entropy does
+    not reach the logits) the gradient is that of lambda * bbar alone, in closed
+    form: d(lambda bbar)/dl_k = (lambda / n) (pi_k / tau) (B_k - sum_j pi_j B_j)."""
+    rng = np.random.default_rng(21)
+    W = rng.standard_normal((2, 256))
+    l = rng.standard_normal((2, 4, 4))
+    e = rng.gumbel(size=(2, 4, 4))
+    tau, lam, n = 0.9, 3.0, 8
+    pi = qat.forward(W, l, e, tau)["pi"]
+    d = qat.logit_grad(W, np.zeros_like(W), pi, tau, lam, n_groups=n)
+    B = np.array([1.0, 2.0, 4.0, 8.0])
+    expect = (lam / n) * (pi / tau) * (B - np.sum(pi * B, axis=-1, keepdims=True))
+    np.testing.assert_allclose(d, expect, rtol=1e-13, atol=1e-15)
+
+
 # ------------------------------------------------------------------ mutations
 
 def _mutant_softmax_times_tau(logits, noise, tau):
