@@ -71,10 +71,9 @@
  *     are returned, a failed launch returns VBQ_ERR_HIP.
  *   - Device pointers must be 16-byte aligned; x / X are contiguous fp16.
  *   - Nothing throws across this interface.
- *   - Environment: VBQ_ONE_WAVE_PER_UNIT=1 makes the one-row GEMV use one wave
- *     per unit everywhere (by default small mixed-width matrices run two waves
- *     per unit).  It exists to test both kernels on the same inputs; results
- *     agree within the output tolerance, bitwise where both take whole units.
+ *   - The library reads no environment variables: every option of a device
+ *     call is a bit of vbq_desc.flags (VBQ_Y_F16, VBQ_ONE_WAVE_PER_UNIT below),
+ *     read once per call.
  */
 #ifndef VBQ_H
 #define VBQ_H
@@ -106,6 +105,26 @@ typedef enum vbq_status {
 #define VBQ_NSECTIONS 10
 #define VBQ_MAX_M 16
 
+/* vbq_desc.flags: options of the device calls that take the descriptor
+ * (vbq_gemv, vbq_gemv_rows, vbq_gemm_small, and the matrices of a step plan),
+ * read on every call.  The packers write 0; set bits on a copy of the
+ * descriptor to choose them.  Other bits give VBQ_ERR_UNSUPPORTED.
+ *   VBQ_Y_F16             y / Y is written as IEEE fp16 (each fp32 result
+ *                         rounded to nearest even): at most 2^-11 relative
+ *                         error added for |y| in [2^-14, 65504], at most 2^-25
+ *                         absolute below that, +-inf from 65520 up.  y / Y must
+ *                         then be 2-byte aligned (4 bytes for float).  Ignored
+ *                         by vbq_dequant.
+ *   VBQ_ONE_WAVE_PER_UNIT the one- and two-row products use one wave per unit
+ *                         even where the library would use two (small
+ *                         mixed-width matrices).  Results agree within the
+ *                         output tolerance, bitwise where both take whole
+ *                         units; it exists so both kernels can be compared on
+ *                         the same inputs. */
+#define VBQ_Y_F16 1u
+#define VBQ_ONE_WAVE_PER_UNIT 2u
+#define VBQ_CALL_FLAGS (VBQ_Y_F16 | VBQ_ONE_WAVE_PER_UNIT)
+
 /* Section indices in vbq_desc.section_off / section_len. */
 enum { VBQ_SEC_UNITS = 0, VBQ_SEC_WMAP = 1, VBQ_SEC_CODES0 = 2, VBQ_SEC_SCALES0 = 6 };
 
@@ -123,7 +142,7 @@ typedef struct vbq_desc {
   uint64_t section_off[VBQ_NSECTIONS];
   uint64_t section_len[VBQ_NSECTIONS];
   uint64_t total_bytes;  /* size of the blob                           */
-  uint32_t flags;        /* reserved, 0                                */
+  uint32_t flags;        /* call options (VBQ_Y_F16, ...); packers write 0 */
   uint32_t reserved1;
 } vbq_desc;
 
@@ -175,12 +194,14 @@ vbq_status vbq_pack_codes(int64_t N, int64_t K, const int8_t* q,
 vbq_status vbq_desc_check(const vbq_desc* d);
 
 /* y[n] = sum_k w_hat[n][k] * x[k]   (fused dequantize + GEMV, paper section 6)
- * blob_dev: the packed blob in device memory (desc->total_bytes bytes);
- * x_dev: device fp16[K]; y_dev: device float32[N].  Asynchronous on stream
- * (a hipStream_t; NULL = default stream).  The sum over each row is taken in
- * a fixed order, so results are bitwise reproducible for a given blob. */
+ * blob_dev: the packed blob in device memory (desc->total_bytes bytes,
+ * 256-byte aligned); x_dev: device fp16[K], 16-byte aligned; y_dev: device
+ * float32[N] (fp16[N] with VBQ_Y_F16).  Asynchronous on stream (a hipStream_t;
+ * NULL = default stream).  The sum over each row is taken in a fixed order, so
+ * results are bitwise reproducible for a given blob.  Errors: NULL, DESC,
+ * BUFFER (misaligned), UNSUPPORTED (unknown flags, blob >= 4 GiB), HIP. */
 vbq_status vbq_gemv(const vbq_desc* desc, const void* blob_dev,
-                    const void* x_dev, float* y_dev, void* stream);
+                    const void* x_dev, void* y_dev, void* stream);
 
 /* Row-bucketed output (paper section 6, "Fused kernels over packed weights":
  * the mixed-precision LM head is stored as a few frequency-grouped row
@@ -194,16 +215,79 @@ vbq_status vbq_gemv(const vbq_desc* desc, const void* blob_dev,
  * buckets of one output may run back to back on one stream.  Errors: NULL,
  * SHAPE (y_len < 0), BUFFER (misaligned pointers), DESC, HIP. */
 vbq_status vbq_gemv_rows(const vbq_desc* desc, const void* blob_dev,
-                         const void* x_dev, float* y_dev, int64_t y_len,
+                         const void* x_dev, void* y_dev, int64_t y_len,
                          const int32_t* row_index_dev, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Row buckets (paper section 6, "Fused kernels over packed weights": the
+ * mixed-precision LM head is stored as a few frequency-grouped row buckets;
+ * section 4: the recipe's head gives each row one width by its token's
+ * frequency rank).  A matrix whose rows each have ONE width is stored as one
+ * packed matrix per width present (a bucket: one width, so no width map), and
+ * each bucket writes its rows of y through vbq_gemv_rows.
+ * ------------------------------------------------------------------------- */
+#define VBQ_MAX_BUCKETS 4
+
+typedef struct vbq_bucket {
+  int32_t bits;          /* the bucket's width: 1, 2, 4 or 8                  */
+  int32_t reserved;      /* 0                                                 */
+  int64_t row_begin;     /* its rows' output indices are                     */
+  int64_t n_rows;        /*   row_index[row_begin .. row_begin + n_rows)      */
+  uint64_t blob_offset;  /* byte offset of its packed matrix in the blob     */
+  vbq_desc desc;         /* its packed matrix: n_rows x K, all of width bits  */
+} vbq_bucket;
+
+/* Bytes of the blob vbq_pack_row_buckets writes, and the number of buckets
+ * (widths present).  row_bits: host uint8[N], the width of every group of
+ * row n, each in {1,2,4,8}.  opts as for vbq_pack (applied to every bucket;
+ * NULL = the library's choice per bucket).  Errors: NULL, SHAPE, BITS,
+ * UNSUPPORTED. */
+vbq_status vbq_pack_row_buckets_size(int64_t N, int64_t K, const uint8_t* row_bits,
+                                     const vbq_pack_opts* opts, size_t* bytes,
+                                     int32_t* n_buckets);
+
+/* Pack a matrix of one width per row as row buckets.  q: host int8[N][K]
+ * levels; scale_f16: host uint16[N][K/64] fp16 scales; row_bits as above.
+ * Bucket i (increasing width) holds the rows of that width in increasing row
+ * order, packed exactly as vbq_pack_codes packs those rows alone (so its bytes
+ * are that call's bytes), at blob + buckets[i].blob_offset (256-byte aligned).
+ * row_index (host int32[N]) receives the rows of bucket 0, then bucket 1, ...
+ * blob: host buffer of blob_bytes >= vbq_pack_row_buckets_size bytes, 8-byte
+ * aligned.  Upload blob and row_index to the device as they are.  Errors:
+ * NULL, SHAPE, BITS, CODE_RANGE, NONFINITE, SCALE_RANGE, BUFFER, UNSUPPORTED. */
+vbq_status vbq_pack_row_buckets(int64_t N, int64_t K, const int8_t* q,
+                                const uint16_t* scale_f16, const uint8_t* row_bits,
+                                const vbq_pack_opts* opts, void* blob,
+                                size_t blob_bytes,
+                                vbq_bucket buckets[VBQ_MAX_BUCKETS],
+                                int32_t* n_buckets, int32_t* row_index);
+
+/* y = w_hat x for a bucketed matrix: vbq_gemv_rows for each bucket in turn on
+ * one stream, bucket i reading blob_dev + buckets[i].blob_offset and writing
+ * rows row_index_dev[row_begin ..].  The bucket descriptors' flags apply.
+ * blob_dev 256-byte aligned; row_index_dev device int32[sum n_rows]; y_dev
+ * device float32[y_len] (fp16 with VBQ_Y_F16).  Errors: as vbq_gemv_rows, and
+ * SHAPE for n_buckets outside [0, VBQ_MAX_BUCKETS]. */
+vbq_status vbq_gemv_buckets(const vbq_bucket* buckets, int32_t n_buckets,
+                            const void* blob_dev, const int32_t* row_index_dev,
+                            const void* x_dev, void* y_dev, int64_t y_len,
+                            void* stream);
 
 /* Y[m][n] = sum_k w_hat[n][k] * X[m][k] for m < M, 0 <= M <= 16
  * (small-batch decode).  X_dev: device fp16 rows with stride ldx >= K
- * elements (ldx % 8 == 0); Y_dev: device float32 rows with stride ldy >= N.
- * M == 0 is a no-op.  Weights are streamed once for all M rows. */
+ * elements (ldx % 8 == 0); Y_dev: device float32 rows (fp16 with VBQ_Y_F16)
+ * with stride ldy >= N elements.  M == 0 is a no-op.  Weights are streamed
+ * once for all M rows. */
 vbq_status vbq_gemm_small(const vbq_desc* desc, const void* blob_dev,
                           int64_t M, const void* X_dev, int64_t ldx,
-                          float* Y_dev, int64_t ldy, void* stream);
+                          void* Y_dev, int64_t ldy, void* stream);
+
+/* Name of the kernel that vbq_gemm_small with M activation rows (vbq_gemv and
+ * vbq_gemv_rows for M = 1) launches on this matrix, e.g.
+ * "vbq_mv_pair_kernel<8,1>" (static storage; "none" for an invalid descriptor
+ * or M outside [1, 16]).  The choice depends on the widths present, the grid
+ * and the flags; a caller or a profile can group launches by it. */
+const char* vbq_kernel_name(const vbq_desc* desc, int64_t M);
 
 /* W_dev[n][k] = w_hat[n][k] = s*q as float32 (exact), device float32[N][K].
  * For checking the packed stream against the quantizer bit for bit. */
@@ -303,6 +387,18 @@ vbq_status vbq_qat_logit_grad(int64_t n_groups, const float* W_dev,
                               const float* grad_dev, const float* pi_dev,
                               float tau, float lambda, int64_t n_bbar,
                               float* dlogits_dev, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Measurement aid of the roofline harness (not part of the method).
+ * ------------------------------------------------------------------------- */
+
+/* Reads `bytes` bytes at src_dev (device, 16-byte aligned, bytes % 16 == 0)
+ * with 16-byte non-temporal loads over `blocks` workgroups of 256 lanes
+ * (0 = 8192), folding them with XOR into sink_dev (device uint32[4 * blocks],
+ * contents meaningless), so the time of the launch is the device's plain
+ * streaming-read rate.  Errors: NULL, BUFFER, UNSUPPORTED (blocks > 2^20), HIP. */
+vbq_status vbq_read_ceiling(const void* src_dev, size_t bytes, uint32_t blocks,
+                            uint32_t* sink_dev, void* stream);
 
 #ifdef __cplusplus
 }

@@ -33,7 +33,7 @@ def _run(cmd, verbose):
 
 
 def build(verbose=False):
-    """Compile the packer (host C++), the decode kernels and the selection kernels (HIP, gfx950) into libvbq.so."""
+    """Compile the packer (host C++), the decode, selection and measurement kernels (HIP, gfx950) into libvbq.so."""
     hipcc = shutil.which("hipcc") or os.path.join(ROCM, "bin", "hipcc")
     clang = os.path.join(ROCM, "llvm", "bin", "clang++")
     if not os.path.exists(clang):
@@ -45,11 +45,14 @@ def build(verbose=False):
           os.path.join(CSRC, "vbq_pack.cpp"), "-o", pack_o], verbose)
     _run([hipcc, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", *DEVICE_FLAGS, "-c",
           os.path.join(CSRC, "vbq_kernels.hip"), "-o", kern_o], verbose)
-    sel_o = os.path.join(BUILD, "vbq_select.o")
-    _run([hipcc, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", *DEVICE_FLAGS, "-c",
-          os.path.join(CSRC, "vbq_select.hip"), "-o", sel_o], verbose)
+    objs = [pack_o, kern_o]
+    for name in ("vbq_select", "vbq_measure"):
+        o = os.path.join(BUILD, name + ".o")
+        _run([hipcc, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", *DEVICE_FLAGS, "-c",
+              os.path.join(CSRC, name + ".hip"), "-o", o], verbose)
+        objs.append(o)
     tmp = LIB + ".tmp"
-    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", pack_o, kern_o, sel_o, "-o", tmp, "-lpthread"], verbose)
+    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp, "-lpthread"], verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -28,7 +28,6 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
-#include <cstdlib>
 #include <cstdint>
 #include <type_traits>
 
@@ -67,24 +66,34 @@ __device__ __forceinline__ T ld_nt(const uint8_t* base, uint32_t off) {
 struct MvArgs {
   DevMatrix m;
   const uint16_t* x;  // fp16 bits, row m at x + m*ldx
-  float* y;           // row m at y + m*ldy
+  void* y;            // row m at y + m*ldy elements (float, or fp16 bits when yf16)
   int64_t ldx, ldy;
   int32_t M;          // rows of x actually present (<= MT)
   int32_t S;          // slices per unit
   int32_t SW;         // group columns per window (LDS staging)
+  int32_t yf16;       // 1: y holds fp16 (each fp32 result rounded to nearest even)
   // one activation row only: output row n goes to y[rows[n]] (skipped unless
   // 0 <= rows[n] < ylen); rows == nullptr writes y[n]
   const int32_t* rows;
   int64_t ylen;
 };
 
+// Element i of y as float, or as fp16 rounded to nearest even (the
+// conversion instruction's default rounding).
+__device__ __forceinline__ void store_y(void* y, size_t i, float v, int32_t f16) {
+  if (f16)
+    ((_Float16*)y)[i] = (_Float16)v;
+  else
+    ((float*)y)[i] = v;
+}
+
 // Stores output row n of a one-row product, through the row map if there is one.
 __device__ __forceinline__ void store_row(const MvArgs& a, size_t n, float v) {
   if (a.rows == nullptr) {
-    a.y[n] = v;
+    store_y(a.y, n, v, a.yf16);
   } else {
     const int64_t d = a.rows[n];
-    if (d >= 0 && d < a.ylen) a.y[d] = v;
+    if (d >= 0 && d < a.ylen) store_y(a.y, (size_t)d, v, a.yf16);
   }
 }
 
@@ -962,7 +971,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       if (MT == 1)
         store_row(a, (size_t)t * R + r, tot);
       else
-        a.y[m * a.ldy + (size_t)t * R + r] = tot;
+        store_y(a.y, m * a.ldy + (size_t)t * R + r, tot, a.yf16);
     }
   }
 }
@@ -1116,7 +1125,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       if constexpr (MT == 1)
         store_row(a, (size_t)t * R + r, tot);
       else
-        a.y[m * a.ldy + (size_t)t * R + r] = tot;
+        store_y(a.y, m * a.ldy + (size_t)t * R + r, tot, a.yf16);
     }
   }
 }
@@ -1150,10 +1159,11 @@ constexpr int kMmMaxCols = 32;  // group columns of a slice
 struct MmArgs {
   DevMatrix m;
   const uint16_t* x;  // fp16 bits, row m at x + m*ldx
-  float* y;           // row m at y + m*ldy
+  void* y;            // row m at y + m*ldy elements (float, or fp16 bits when yf16)
   int64_t ldx, ldy;
   int32_t M;          // rows of X (3..16)
   int32_t S;          // slices per unit
+  int32_t yf16;       // 1: y holds fp16
 };
 
 // Bytes of one wave's LDS region: row sums (16 x R floats) and the
@@ -1365,7 +1375,7 @@ __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(const uint8_t* __restri
       float tot = 0.0f;
 #pragma unroll
       for (int w2 = 0; w2 < NW; ++w2) tot += lds_f32(lds0 + (uint32_t)(w2 * wbytes) + 4u * (uint32_t)slot);
-      a.y[m * a.ldy + (size_t)t * R + r] = tot;
+      store_y(a.y, m * a.ldy + (size_t)t * R + r, tot, a.yf16);
     }
   }
 }
@@ -1438,6 +1448,7 @@ vbq_status make_dev_matrix(const vbq_desc* d, const void* blob, DevMatrix* m) {
   if (d->total_bytes >= (1ull << 32)) return VBQ_ERR_UNSUPPORTED;  // 32-bit section offsets
   // the kernels address the unit table at offset 0 (the layout's first section)
   if (d->section_off[VBQ_SEC_UNITS] != 0) return VBQ_ERR_DESC;
+  if (d->flags & ~(uint32_t)VBQ_CALL_FLAGS) return VBQ_ERR_UNSUPPORTED;
   m->blob = (const uint8_t*)blob;
   m->off_units = 0;
   m->off_wmap = (uint32_t)d->section_off[VBQ_SEC_WMAP];
@@ -1584,20 +1595,28 @@ vbq_status launch_pair_nw(const MvArgs& a, int lds, hipStream_t s) {
 
 // Launches the pair kernel for MT (1 or 2) activation rows when the matrix
 // qualifies; *used says whether it did.
-template <int MT>
-vbq_status try_launch_pair(const DevMatrix& m, const void* x, int64_t ldx, float* y, int64_t ldy, const int32_t* rows,
-                           int64_t ylen, hipStream_t s, bool* used) {
-  *used = false;
+// Waves per workgroup of the pair kernel for MT activation rows, or 0 when
+// the matrix does not qualify.
+int pair_waves(const DevMatrix& m, int MT) {
   int classes = 0;
   for (int c = 0; c < 4; ++c) classes += m.n_entries[c] ? 1 : 0;
-  if (classes < 2 || m.U < 2 || m.U > 8 || m.C > kXRegs * 8) return VBQ_OK;
+  if (classes < 2 || m.U < 2 || m.U > 8 || m.C > kXRegs * 8) return 0;
   // (two rows: a grid half as large, beyond which the one-wave kernel is faster)
-  if ((int64_t)m.T * m.U > (MT == 1 ? kPairMaxUnits : kPairMaxUnits / 2)) return VBQ_OK;
+  if ((int64_t)m.T * m.U > (MT == 1 ? kPairMaxUnits : kPairMaxUnits / 2)) return 0;
   // two rows fit the registers of 8 waves per workgroup (2 per SIMD), not of 16
-  if (MT > 1 && m.U > 4) return VBQ_OK;
+  if (MT > 1 && m.U > 4) return 0;
   const int NW = m.U <= 4 ? 8 : 16;
   const int lds = (NW / 2) * (MT * m.R * 4 + wave_plan(m.R, m.C, MT).bytes);
-  if (lds > kLdsLimit) return VBQ_OK;
+  return lds > kLdsLimit ? 0 : NW;
+}
+
+template <int MT>
+vbq_status try_launch_pair(const DevMatrix& m, const void* x, int64_t ldx, void* y, int64_t ldy, bool yf16,
+                           const int32_t* rows, int64_t ylen, hipStream_t s, bool* used) {
+  *used = false;
+  const int NW = pair_waves(m, MT);
+  if (NW == 0) return VBQ_OK;
+  const int lds = (NW / 2) * (MT * m.R * 4 + wave_plan(m.R, m.C, MT).bytes);
   MvArgs a;
   a.m = m;
   a.x = (const uint16_t*)x;
@@ -1607,6 +1626,7 @@ vbq_status try_launch_pair(const DevMatrix& m, const void* x, int64_t ldx, float
   a.M = MT;
   a.S = 1;
   a.SW = m.C;
+  a.yf16 = yf16 ? 1 : 0;
   a.rows = MT == 1 ? rows : nullptr;
   a.ylen = ylen;
   *used = true;
@@ -1615,16 +1635,15 @@ vbq_status try_launch_pair(const DevMatrix& m, const void* x, int64_t ldx, float
   return launch_pair_nw<8, MT>(a, lds, s);
 }
 
+// flags: the descriptor's call options (VBQ_Y_F16, VBQ_ONE_WAVE_PER_UNIT).
 template <int MT>
-vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, float* y, int64_t ldy, hipStream_t s,
-                     const int32_t* rows = nullptr, int64_t ylen = 0) {
+vbq_status launch_mv(const DevMatrix& m, uint32_t flags, const void* x, int64_t ldx, int M, void* y, int64_t ldy,
+                     hipStream_t s, const int32_t* rows = nullptr, int64_t ylen = 0) {
+  const bool yf16 = (flags & VBQ_Y_F16) != 0;
   if constexpr (MT <= 2) {
-    // VBQ_ONE_WAVE_PER_UNIT=1 turns the pair kernel off (to test both paths
-    // on the same inputs)
-    const char* one = getenv("VBQ_ONE_WAVE_PER_UNIT");
-    if (!(one && one[0] == '1')) {
+    if (!(flags & VBQ_ONE_WAVE_PER_UNIT)) {
       bool used = false;
-      const vbq_status st = try_launch_pair<MT>(m, x, ldx, y, ldy, rows, ylen, s, &used);
+      const vbq_status st = try_launch_pair<MT>(m, x, ldx, y, ldy, yf16, rows, ylen, s, &used);
       if (used) return st;
     }
   }
@@ -1639,6 +1658,7 @@ vbq_status launch_mv(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
   a.M = M;
   a.S = sh.S;
   a.SW = sh.SW;
+  a.yf16 = yf16 ? 1 : 0;
   a.rows = MT == 1 ? rows : nullptr;
   a.ylen = ylen;
   if constexpr (MT == 1) {
@@ -1700,10 +1720,11 @@ vbq_status launch_mm_rb(const MmArgs& a, int NW, int lds, hipStream_t s) {
   return launch_mm_nw<16, RB>(a, lds, s);
 }
 
-vbq_status launch_mm(const DevMatrix& m, const void* x, int64_t ldx, int M, float* y, int64_t ldy, hipStream_t s) {
-  // Each wave walks its blocks one after the other, so small matrices split
-  // their tiles over more waves, as long as the whole grid fits the GPU at
-  // once (about 20 waves per CU at this kernel's register use).
+// Launch shape of the matrix-core kernel: waves per workgroup, slices per
+// unit, LDS bytes.  Each wave walks its blocks one after the other, so small
+// matrices split their tiles over more waves, as long as the whole grid fits
+// the GPU at once (about 20 waves per CU at this kernel's register use).
+bool mm_shape(const DevMatrix& m, int* NWo, int* So, int* ldso) {
   int NWt = kMinWaves;
   while (NWt < 16 && (int64_t)m.T * NWt * 2 <= 256 * 20) NWt *= 2;
   int S = (NWt + m.U - 1) / m.U;
@@ -1711,8 +1732,16 @@ vbq_status launch_mm(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
   const int wbytes = mm_wave_bytes(m.R, max_slice_cols(m.R, m.C, S));
   int NW = kMinWaves;  // (fewer waves than items is fine: items are dealt in turn)
   while (NW < 16 && NW < m.U * S && 2 * NW * wbytes <= kLdsLimit) NW *= 2;
-  const int lds = NW * wbytes;
-  if (lds > kLdsLimit) return VBQ_ERR_UNSUPPORTED;
+  *NWo = NW;
+  *So = S;
+  *ldso = NW * wbytes;
+  return NW * wbytes <= kLdsLimit;
+}
+
+vbq_status launch_mm(const DevMatrix& m, uint32_t flags, const void* x, int64_t ldx, int M, void* y, int64_t ldy,
+                     hipStream_t s) {
+  int NW, S, lds;
+  if (!mm_shape(m, &NW, &S, &lds)) return VBQ_ERR_UNSUPPORTED;
   MmArgs a;
   a.m = m;
   a.x = (const uint16_t*)x;
@@ -1721,10 +1750,51 @@ vbq_status launch_mm(const DevMatrix& m, const void* x, int64_t ldx, int M, floa
   a.ldy = ldy;
   a.M = M;
   a.S = S;
+  a.yf16 = (flags & VBQ_Y_F16) ? 1 : 0;
   // row blocks of 16 per group: one, two or four (R = 16, 32, >= 64)
   if (m.R == 16) return launch_mm_rb<1>(a, NW, lds, s);
   if (m.R == 32) return launch_mm_rb<2>(a, NW, lds, s);
   return launch_mm_rb<4>(a, NW, lds, s);
+}
+
+// Name of the kernel a product with M activation rows launches on this matrix
+// (the same choices as launch_mv / launch_mm); static storage.
+const char* kernel_name(const DevMatrix& m, uint32_t flags, int M) {
+  static const char* const kNames[] = {
+      "vbq_mv_pair_kernel<8,1>", "vbq_mv_pair_kernel<16,1>", "vbq_mv_pair_kernel<8,2>",
+      "vbq_mv_kernel<1,4>", "vbq_mv_kernel<1,8>", "vbq_mv_kernel<1,16>",
+      "vbq_mv_kernel<2,4>", "vbq_mv_kernel<2,8>",
+      "vbq_mv_kernel<1,4,1-bit>", "vbq_mv_kernel<1,8,1-bit>", "vbq_mv_kernel<1,16,1-bit>",
+      "vbq_mv_kernel<1,4,2-bit>", "vbq_mv_kernel<1,8,2-bit>", "vbq_mv_kernel<1,16,2-bit>",
+      "vbq_mv_kernel<1,4,4-bit>", "vbq_mv_kernel<1,8,4-bit>", "vbq_mv_kernel<1,16,4-bit>",
+      "vbq_mv_kernel<1,4,8-bit>", "vbq_mv_kernel<1,8,8-bit>", "vbq_mv_kernel<1,16,8-bit>",
+      "vbq_mm_kernel<4,16-row blocks>", "vbq_mm_kernel<8,16-row blocks>", "vbq_mm_kernel<16,16-row blocks>",
+      "vbq_mm_kernel<4,32-row blocks>", "vbq_mm_kernel<8,32-row blocks>", "vbq_mm_kernel<16,32-row blocks>",
+      "vbq_mm_kernel<4,64-row blocks>", "vbq_mm_kernel<8,64-row blocks>", "vbq_mm_kernel<16,64-row blocks>",
+      "none"};
+  auto nw_index = [](int NW) { return NW == 4 ? 0 : NW == 8 ? 1 : 2; };
+  if (M <= 0) return kNames[29];
+  if (M <= 2) {
+    if (!(flags & VBQ_ONE_WAVE_PER_UNIT)) {
+      const int pw = pair_waves(m, M);
+      if (pw) return kNames[M == 2 ? 2 : pw == 8 ? 0 : 1];
+    }
+    MvShape sh;
+    if (!choose_shape(m, M, &sh)) return kNames[29];
+    if (M == 2) return kNames[sh.NW == 4 ? 6 : 7];
+    int uni = -1, classes = 0;
+    for (int c = 0; c < 4; ++c)
+      if (m.n_entries[c]) {
+        uni = c;
+        ++classes;
+      }
+    if (classes == 1) return kNames[8 + 3 * uni + nw_index(sh.NW)];
+    return kNames[3 + nw_index(sh.NW)];
+  }
+  int NW, S, lds;
+  if (!mm_shape(m, &NW, &S, &lds)) return kNames[29];
+  const int rb = m.R == 16 ? 0 : m.R == 32 ? 1 : 2;
+  return kNames[20 + 3 * rb + nw_index(NW)];
 }
 
 }  // namespace
@@ -1737,28 +1807,48 @@ extern "C" {
 
 const char* vbq_last_hip_error(void) { return hipGetErrorName(g_last_hip_error); }
 
-vbq_status vbq_gemv(const vbq_desc* desc, const void* blob_dev, const void* x_dev, float* y_dev, void* stream) {
+// Required alignment of y: 4 bytes for float, 2 for fp16.
+inline uintptr_t y_align(const vbq_desc* d) { return (d->flags & VBQ_Y_F16) ? 2 : 4; }
+
+vbq_status vbq_gemv(const vbq_desc* desc, const void* blob_dev, const void* x_dev, void* y_dev, void* stream) {
   if (!x_dev || !y_dev) return VBQ_ERR_NULL;
   DevMatrix m;
   vbq_status st = make_dev_matrix(desc, blob_dev, &m);
   if (st != VBQ_OK) return st;
-  if ((uintptr_t)x_dev % 16 || (uintptr_t)y_dev % 4) return VBQ_ERR_BUFFER;
-  return launch_mv<1>(m, x_dev, desc->K, 1, y_dev, desc->N, (hipStream_t)stream);
+  if ((uintptr_t)x_dev % 16 || (uintptr_t)y_dev % y_align(desc)) return VBQ_ERR_BUFFER;
+  return launch_mv<1>(m, desc->flags, x_dev, desc->K, 1, y_dev, desc->N, (hipStream_t)stream);
 }
 
-vbq_status vbq_gemv_rows(const vbq_desc* desc, const void* blob_dev, const void* x_dev, float* y_dev, int64_t y_len,
+vbq_status vbq_gemv_rows(const vbq_desc* desc, const void* blob_dev, const void* x_dev, void* y_dev, int64_t y_len,
                          const int32_t* row_index_dev, void* stream) {
   if (!x_dev || !y_dev || !row_index_dev) return VBQ_ERR_NULL;
   if (y_len < 0) return VBQ_ERR_SHAPE;
   DevMatrix m;
   vbq_status st = make_dev_matrix(desc, blob_dev, &m);
   if (st != VBQ_OK) return st;
-  if ((uintptr_t)x_dev % 16 || (uintptr_t)y_dev % 4 || (uintptr_t)row_index_dev % 4) return VBQ_ERR_BUFFER;
-  return launch_mv<1>(m, x_dev, desc->K, 1, y_dev, desc->N, (hipStream_t)stream, row_index_dev, y_len);
+  if ((uintptr_t)x_dev % 16 || (uintptr_t)y_dev % y_align(desc) || (uintptr_t)row_index_dev % 4)
+    return VBQ_ERR_BUFFER;
+  return launch_mv<1>(m, desc->flags, x_dev, desc->K, 1, y_dev, desc->N, (hipStream_t)stream, row_index_dev, y_len);
+}
+
+vbq_status vbq_gemv_buckets(const vbq_bucket* buckets, int32_t n_buckets, const void* blob_dev,
+                            const int32_t* row_index_dev, const void* x_dev, void* y_dev, int64_t y_len,
+                            void* stream) {
+  if (n_buckets < 0 || n_buckets > VBQ_MAX_BUCKETS) return VBQ_ERR_SHAPE;
+  if (n_buckets == 0) return VBQ_OK;
+  if (!buckets || !blob_dev || !row_index_dev) return VBQ_ERR_NULL;
+  for (int32_t i = 0; i < n_buckets; ++i) {
+    const vbq_bucket& b = buckets[i];
+    if (b.row_begin < 0 || b.n_rows != b.desc.N) return VBQ_ERR_DESC;
+    const vbq_status st = vbq_gemv_rows(&b.desc, (const uint8_t*)blob_dev + b.blob_offset, x_dev, y_dev, y_len,
+                                        row_index_dev + b.row_begin, stream);
+    if (st != VBQ_OK) return st;
+  }
+  return VBQ_OK;
 }
 
 vbq_status vbq_gemm_small(const vbq_desc* desc, const void* blob_dev, int64_t M, const void* X_dev, int64_t ldx,
-                          float* Y_dev, int64_t ldy, void* stream) {
+                          void* Y_dev, int64_t ldy, void* stream) {
   if (M < 0 || M > VBQ_MAX_M) return VBQ_ERR_SHAPE;
   DevMatrix m;
   vbq_status st = make_dev_matrix(desc, blob_dev, &m);
@@ -1766,12 +1856,21 @@ vbq_status vbq_gemm_small(const vbq_desc* desc, const void* blob_dev, int64_t M,
   if (M == 0) return VBQ_OK;
   if (!X_dev || !Y_dev) return VBQ_ERR_NULL;
   if (ldx < desc->K || ldx % 8 || ldy < desc->N) return VBQ_ERR_SHAPE;
-  if ((uintptr_t)X_dev % 16 || (uintptr_t)Y_dev % 4) return VBQ_ERR_BUFFER;
+  if ((uintptr_t)X_dev % 16 || (uintptr_t)Y_dev % y_align(desc)) return VBQ_ERR_BUFFER;
   hipStream_t s = (hipStream_t)stream;
   const int Mi = (int)M;
-  if (Mi == 1) return launch_mv<1>(m, X_dev, ldx, 1, Y_dev, ldy, s);
-  if (Mi == 2) return launch_mv<2>(m, X_dev, ldx, 2, Y_dev, ldy, s);
-  return launch_mm(m, X_dev, ldx, Mi, Y_dev, ldy, s);
+  const uint32_t f = desc->flags;
+  if (Mi == 1) return launch_mv<1>(m, f, X_dev, ldx, 1, Y_dev, ldy, s);
+  if (Mi == 2) return launch_mv<2>(m, f, X_dev, ldx, 2, Y_dev, ldy, s);
+  return launch_mm(m, f, X_dev, ldx, Mi, Y_dev, ldy, s);
+}
+
+const char* vbq_kernel_name(const vbq_desc* desc, int64_t M) {
+  DevMatrix m;
+  // (any aligned non-null address: only the descriptor is looked at)
+  if (!desc || make_dev_matrix(desc, (const void*)(uintptr_t)256, &m) != VBQ_OK || M < 0 || M > VBQ_MAX_M)
+    return "none";
+  return kernel_name(m, desc->flags, (int)M);
 }
 
 vbq_status vbq_dequant(const vbq_desc* desc, const void* blob_dev, float* W_dev, void* stream) {

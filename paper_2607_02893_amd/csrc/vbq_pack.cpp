@@ -336,6 +336,106 @@ vbq_status vbq_pack_codes(int64_t N, int64_t K, const int8_t* q, const uint16_t*
   return pack_impl(N, K, src, bits, opts, blob, blob_bytes, desc);
 }
 
+namespace {
+
+// Rows of each width in increasing row order, and the widths present.
+vbq_status bucket_rows(int64_t N, const uint8_t* row_bits, std::vector<int64_t> rows[4]) {
+  for (int64_t n = 0; n < N; ++n) {
+    const int c = class_of_bits(row_bits[n]);
+    if (c < 0) return VBQ_ERR_BITS;
+    rows[c].push_back(n);
+  }
+  return VBQ_OK;
+}
+
+// Descriptor and byte size of one bucket (n rows of width 2^c, K columns).
+vbq_status bucket_desc(int64_t n, int64_t K, int c, const vbq_pack_opts* opts, vbq_desc* d) {
+  Geometry g;
+  vbq_status st = make_geometry(n, K, opts, &g);
+  if (st != VBQ_OK) return st;
+  int64_t n_entries[4] = {0, 0, 0, 0};
+  n_entries[c] = n * g.G;
+  if (n_entries[c] > 0xFFFFFFFFll || g.wmap_words > 0xFFFFFFFFll) return VBQ_ERR_UNSUPPORTED;
+  fill_desc_header(g, n_entries, d);
+  return VBQ_OK;
+}
+
+}  // namespace
+
+vbq_status vbq_pack_row_buckets_size(int64_t N, int64_t K, const uint8_t* row_bits, const vbq_pack_opts* opts,
+                                     size_t* bytes, int32_t* n_buckets) {
+  if (!row_bits || !bytes || !n_buckets) return VBQ_ERR_NULL;
+  if (N < 1 || K < kGroup || K % kGroup != 0) return VBQ_ERR_SHAPE;
+  if (opts && opts->flags != 0) return VBQ_ERR_UNSUPPORTED;
+  std::vector<int64_t> rows[4];
+  vbq_status st = bucket_rows(N, row_bits, rows);
+  if (st != VBQ_OK) return st;
+  uint64_t total = 0;
+  int32_t nb = 0;
+  for (int c = 0; c < 4; ++c) {
+    if (rows[c].empty()) continue;
+    vbq_desc d;
+    if ((st = bucket_desc((int64_t)rows[c].size(), K, c, opts, &d)) != VBQ_OK) return st;
+    total = align_up(total) + d.total_bytes;
+    ++nb;
+  }
+  *bytes = (size_t)total;
+  *n_buckets = nb;
+  return VBQ_OK;
+}
+
+vbq_status vbq_pack_row_buckets(int64_t N, int64_t K, const int8_t* q, const uint16_t* scale_f16,
+                                const uint8_t* row_bits, const vbq_pack_opts* opts, void* blob, size_t blob_bytes,
+                                vbq_bucket buckets[VBQ_MAX_BUCKETS], int32_t* n_buckets, int32_t* row_index) {
+  if (!q || !scale_f16 || !row_bits || !blob || !buckets || !n_buckets || !row_index) return VBQ_ERR_NULL;
+  size_t need = 0;
+  int32_t nb = 0;
+  vbq_status st = vbq_pack_row_buckets_size(N, K, row_bits, opts, &need, &nb);
+  if (st != VBQ_OK) return st;
+  if ((uintptr_t)blob % 8 != 0 || blob_bytes < need) return VBQ_ERR_BUFFER;
+  std::vector<int64_t> rows[4];
+  bucket_rows(N, row_bits, rows);
+  const int64_t G = K / kGroup;
+  uint64_t off = 0;
+  int64_t row_begin = 0;
+  int32_t i = 0;
+  std::vector<int8_t> qb;
+  std::vector<uint16_t> sb;
+  std::vector<uint8_t> bb;
+  for (int c = 0; c < 4; ++c) {
+    const int64_t n = (int64_t)rows[c].size();
+    if (n == 0) continue;
+    // the bucket's rows, gathered in order: the same input vbq_pack_codes
+    // would get for these rows alone
+    qb.resize((size_t)(n * K));
+    sb.resize((size_t)(n * G));
+    bb.assign((size_t)(n * G), (uint8_t)(1u << c));
+    for (int64_t r = 0; r < n; ++r) {
+      const int64_t src = rows[c][(size_t)r];
+      std::memcpy(&qb[(size_t)(r * K)], q + src * K, (size_t)K);
+      std::memcpy(&sb[(size_t)(r * G)], scale_f16 + src * G, (size_t)G * 2);
+      row_index[row_begin + r] = (int32_t)src;
+    }
+    off = align_up(off);
+    vbq_bucket& b = buckets[i];
+    b = vbq_bucket{};
+    b.bits = 1 << c;
+    b.row_begin = row_begin;
+    b.n_rows = n;
+    b.blob_offset = off;
+    Source src;
+    src.q = qb.data();
+    src.scales = sb.data();
+    st = pack_impl(n, K, src, bb.data(), opts, (uint8_t*)blob + off, blob_bytes - off, &b.desc);
+    if (st != VBQ_OK) return st;
+    off += b.desc.total_bytes;
+    row_begin += n;
+    ++i;
+  }
+  *n_buckets = nb;
+  return VBQ_OK;
+}
+
 vbq_status vbq_desc_check(const vbq_desc* d) {
   if (!d) return VBQ_ERR_NULL;
   if (d->magic != VBQ_MAGIC || d->version != VBQ_LAYOUT_VERSION || d->group != kGroup) return VBQ_ERR_DESC;

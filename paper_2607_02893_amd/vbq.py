@@ -55,8 +55,13 @@ STATUS = {0: "VBQ_OK", 1: "VBQ_ERR_NULL", 2: "VBQ_ERR_SHAPE", 3: "VBQ_ERR_BITS",
           9: "VBQ_ERR_HIP", 10: "VBQ_ERR_UNSUPPORTED"}
 # exported symbols, in the order include/vbq.h declares them
 EXPORTS = ("vbq_status_string", "vbq_last_hip_error", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
-           "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_gemm_small", "vbq_dequant",
-           "vbq_qat_workspace_size", "vbq_qat_forward", "vbq_qat_logit_grad")
+           "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_pack_row_buckets_size", "vbq_pack_row_buckets",
+           "vbq_gemv_buckets", "vbq_gemm_small", "vbq_kernel_name", "vbq_dequant",
+           "vbq_qat_workspace_size", "vbq_qat_forward", "vbq_qat_logit_grad", "vbq_read_ceiling")
+# vbq_desc.flags (call options)
+Y_F16 = 1
+ONE_WAVE_PER_UNIT = 2
+MAX_BUCKETS = 4
 QAT_MAX_GROUPS = 1 << 40
 QAT_WSOFT_BF16 = 1
 QAT_CANDIDATES = (1, 2, 4, 8)
@@ -78,6 +83,11 @@ class VbqDesc(ctypes.Structure):
                 "T": self.n_tiles, "U": self.n_chunks, "units": self.n_units,
                 "n_entries": list(self.n_entries), "section_off": list(self.section_off),
                 "section_len": list(self.section_len), "total_bytes": self.total_bytes}
+
+
+class VbqBucket(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_int32), ("reserved", ctypes.c_int32), ("row_begin", ctypes.c_int64),
+                ("n_rows", ctypes.c_int64), ("blob_offset", ctypes.c_uint64), ("desc", VbqDesc)]
 
 
 class VbqPackOpts(ctypes.Structure):
@@ -107,9 +117,21 @@ _lib.vbq_gemv.restype = ctypes.c_int
 _lib.vbq_gemv.argtypes = [ctypes.POINTER(VbqDesc), _P, _P, _P, _P]
 _lib.vbq_gemv_rows.restype = ctypes.c_int
 _lib.vbq_gemv_rows.argtypes = [ctypes.POINTER(VbqDesc), _P, _P, _P, ctypes.c_int64, _P, _P]
+_lib.vbq_pack_row_buckets_size.restype = ctypes.c_int
+_lib.vbq_pack_row_buckets_size.argtypes = [ctypes.c_int64, ctypes.c_int64, _P, ctypes.POINTER(VbqPackOpts),
+                                           ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_int32)]
+_lib.vbq_pack_row_buckets.restype = ctypes.c_int
+_lib.vbq_pack_row_buckets.argtypes = [ctypes.c_int64, ctypes.c_int64, _P, _P, _P, ctypes.POINTER(VbqPackOpts), _P,
+                                      ctypes.c_size_t, ctypes.POINTER(VbqBucket), ctypes.POINTER(ctypes.c_int32), _P]
+_lib.vbq_gemv_buckets.restype = ctypes.c_int
+_lib.vbq_gemv_buckets.argtypes = [ctypes.POINTER(VbqBucket), ctypes.c_int32, _P, _P, _P, _P, ctypes.c_int64, _P]
 _lib.vbq_gemm_small.restype = ctypes.c_int
 _lib.vbq_gemm_small.argtypes = [ctypes.POINTER(VbqDesc), _P, ctypes.c_int64, _P, ctypes.c_int64, _P,
                                 ctypes.c_int64, _P]
+_lib.vbq_kernel_name.restype = ctypes.c_char_p
+_lib.vbq_kernel_name.argtypes = [ctypes.POINTER(VbqDesc), ctypes.c_int64]
+_lib.vbq_read_ceiling.restype = ctypes.c_int
+_lib.vbq_read_ceiling.argtypes = [_P, ctypes.c_size_t, ctypes.c_uint32, _P, _P]
 _lib.vbq_dequant.restype = ctypes.c_int
 _lib.vbq_dequant.argtypes = [ctypes.POINTER(VbqDesc), _P, _P, _P]
 _lib.vbq_qat_workspace_size.restype = ctypes.c_int
@@ -197,28 +219,60 @@ def pack_codes(q, scales, bits, tile_rows=0, chunk_groups=0, n_threads=0):
     return blob, d
 
 
+def pack_row_buckets_raw(q, scales, row_bits, tile_rows=0, chunk_groups=0, n_threads=0):
+    """vbq_pack_row_buckets: (blob, [VbqBucket], row_index int32[N]) for levels
+    q int8[N][K], fp16 scale bits uint16[N][K/64] and one width per row."""
+    q = np.ascontiguousarray(q, dtype=np.int8)
+    scales = np.ascontiguousarray(scales, dtype=np.uint16)
+    row_bits = np.ascontiguousarray(row_bits, dtype=np.uint8)
+    N, K = q.shape
+    o = _opts(tile_rows, chunk_groups, n_threads)
+    nbytes = ctypes.c_size_t(0)
+    nb = ctypes.c_int32(0)
+    _check(_lib.vbq_pack_row_buckets_size(N, K, _ptr(row_bits), ctypes.byref(o), ctypes.byref(nbytes),
+                                          ctypes.byref(nb)), "vbq_pack_row_buckets_size")
+    blob = _blob(nbytes.value)
+    bk = (VbqBucket * MAX_BUCKETS)()
+    row_index = np.empty(N, dtype=np.int32)
+    _check(_lib.vbq_pack_row_buckets(N, K, _ptr(q), _ptr(scales), _ptr(row_bits), ctypes.byref(o), _ptr(blob),
+                                     nbytes.value, bk, ctypes.byref(nb), _ptr(row_index)), "vbq_pack_row_buckets")
+    return blob, [bk[i] for i in range(nb.value)], row_index
+
+
 def pack_row_buckets(q, scales, bits, tile_rows=0, chunk_groups=0, n_threads=0):
     """Pack a matrix whose rows each have one width (a recipe head: paper section
     4, frequency-tiered rows; section 6, stored as frequency-grouped row buckets)
-    as one packed matrix per width.  Returns [(width, rows, blob, desc)] in
-    increasing width, rows the int32 output rows of the bucket's members in
-    order.  Each bucket has one width, so it carries no width map."""
-    q = np.ascontiguousarray(q, dtype=np.int8)
-    scales = np.ascontiguousarray(scales, dtype=np.uint16)
+    as one packed matrix per width (vbq_pack_row_buckets).  Returns
+    [(width, rows, blob, desc)] in increasing width, rows the int32 output rows
+    of the bucket's members in order and blob that bucket's bytes.  Each bucket
+    has one width, so it carries no width map."""
     bits = np.ascontiguousarray(bits, dtype=np.uint8)
     w = bits[:, 0]
     if not np.array_equal(bits, np.repeat(w[:, None], bits.shape[1], axis=1)):
         raise ValueError("row buckets need one width per row")
+    blob, bk, row_index = pack_row_buckets_raw(q, scales, w, tile_rows, chunk_groups, n_threads)
     out = []
-    for b in np.unique(w):
-        rows = np.nonzero(w == b)[0].astype(np.int32)
-        blob, d = pack_codes(q[rows], scales[rows], bits[rows], tile_rows, chunk_groups, n_threads)
-        out.append((int(b), rows, blob, d))
+    for b in bk:
+        off, n = int(b.blob_offset), int(b.n_rows)
+        d = VbqDesc.from_buffer_copy(b.desc)
+        out.append((int(b.bits), row_index[b.row_begin:b.row_begin + n].copy(),
+                    blob[off:off + int(d.total_bytes)], d))
     return out
 
 
 def desc_check(d):
     return _lib.vbq_desc_check(ctypes.byref(d))
+
+
+def kernel_name(d, M=1):
+    """Name of the kernel a product with M activation rows launches on this matrix."""
+    return _lib.vbq_kernel_name(ctypes.byref(d), int(M)).decode()
+
+
+def raw_read_ceiling(src_ptr, nbytes, blocks, sink_ptr, stream_ptr):
+    """vbq_read_ceiling on raw device addresses."""
+    return _lib.vbq_read_ceiling(ctypes.c_void_p(src_ptr), int(nbytes), int(blocks), ctypes.c_void_p(sink_ptr),
+                                 ctypes.c_void_p(stream_ptr))
 
 
 # ------------------------------------------------------------------ device side
@@ -263,34 +317,53 @@ class PackedMatrix:
     def nbytes(self):
         return int(self.desc.total_bytes)
 
-    def gemv(self, x, y=None, stream=None):
-        """y[N] (float32) = w_hat @ x, x a contiguous fp16 device tensor of length K."""
+    def call_desc(self, y_dtype=None, one_wave_per_unit=False):
+        """A copy of the descriptor with the call options set: fp16 output
+        (y_dtype torch.float16) and one wave per unit."""
+        import torch
+        d = VbqDesc.from_buffer_copy(self.desc)
+        d.flags = (Y_F16 if y_dtype == torch.float16 else 0) | (ONE_WAVE_PER_UNIT if one_wave_per_unit else 0)
+        return d
+
+    def gemv(self, x, y=None, stream=None, y_dtype=None, one_wave_per_unit=False):
+        """y[N] = w_hat @ x, x a contiguous fp16 device tensor of length K; y float32,
+        or float16 (VBQ_Y_F16: the fp32 result rounded to nearest even) when
+        y_dtype or the given y says so."""
         import torch
         dev = self.blob.device
         _need(x, "x", torch.float16, self.K, dev)
+        y_dtype = (y.dtype if y is not None else torch.float32) if y_dtype is None else y_dtype
+        if y_dtype not in (torch.float32, torch.float16):
+            raise ValueError("y must be float32 or float16")
         if y is None:
-            y = torch.empty(self.N, dtype=torch.float32, device=dev)
-        _need(y, "y", torch.float32, self.N, dev)
-        _check(_lib.vbq_gemv(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()),
+            y = torch.empty(self.N, dtype=y_dtype, device=dev)
+        _need(y, "y", y_dtype, self.N, dev)
+        d = self.call_desc(y_dtype, one_wave_per_unit)
+        _check(_lib.vbq_gemv(ctypes.byref(d), ctypes.c_void_p(self.blob.data_ptr()),
                              ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()),
                              _stream_handle(stream)), "vbq_gemv")
         return y
 
     def gemv_rows(self, x, y, rows, stream=None):
         """y[rows[n]] = (w_hat @ x)[n] for every n (indices outside y are not written): one row
-        bucket of a bucketed matrix.  y: float32 device tensor; rows: int32 device tensor of length N."""
+        bucket of a bucketed matrix.  y: float32 (or float16) device tensor; rows: int32 device tensor
+        of length N."""
         import torch
         dev = self.blob.device
         _need(x, "x", torch.float16, self.K, dev)
-        _need(y, "y", torch.float32, None, dev)
+        if y.dtype not in (torch.float32, torch.float16):
+            raise ValueError("y must be float32 or float16")
+        _need(y, "y", y.dtype, None, dev)
         _need(rows, "rows", torch.int32, self.N, dev)
-        _check(_lib.vbq_gemv_rows(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()),
+        d = self.call_desc(y.dtype)
+        _check(_lib.vbq_gemv_rows(ctypes.byref(d), ctypes.c_void_p(self.blob.data_ptr()),
                                   ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()), y.numel(),
                                   ctypes.c_void_p(rows.data_ptr()), _stream_handle(stream)), "vbq_gemv_rows")
         return y
 
-    def gemm_small(self, X, Y=None, stream=None):
-        """Y[M][N] (float32) = X @ w_hat^T for an fp16 device tensor X[M][K], M <= 16."""
+    def gemm_small(self, X, Y=None, stream=None, y_dtype=None, one_wave_per_unit=False):
+        """Y[M][N] = X @ w_hat^T for an fp16 device tensor X[M][K], M <= 16 (rows may be
+        padded: X.stride(0) >= K); Y float32, or float16 when y_dtype or the given Y says so."""
         import torch
         dev = self.blob.device
         if not getattr(X, "is_cuda", False) or X.device != dev:
@@ -298,12 +371,15 @@ class PackedMatrix:
         if X.dtype != torch.float16 or X.dim() != 2 or X.shape[1] != self.K or X.stride(1) != 1:
             raise ValueError("X must be a float16 [M, K] tensor with unit column stride")
         M = X.shape[0]
+        y_dtype = (Y.dtype if Y is not None else torch.float32) if y_dtype is None else y_dtype
         if Y is None:
-            Y = torch.empty((M, self.N), dtype=torch.float32, device=dev)
-        if (not getattr(Y, "is_cuda", False) or Y.device != dev or Y.dtype != torch.float32 or Y.dim() != 2
+            Y = torch.empty((M, self.N), dtype=y_dtype, device=dev)
+        if (not getattr(Y, "is_cuda", False) or Y.device != dev or Y.dtype != y_dtype
+                or y_dtype not in (torch.float32, torch.float16) or Y.dim() != 2
                 or Y.shape[0] != M or Y.shape[1] != self.N or Y.stride(1) != 1):
-            raise ValueError(f"Y must be a float32 [M, N] GPU tensor on {dev} with unit column stride")
-        _check(_lib.vbq_gemm_small(ctypes.byref(self.desc), ctypes.c_void_p(self.blob.data_ptr()), M,
+            raise ValueError(f"Y must be a float32/float16 [M, N] GPU tensor on {dev} with unit column stride")
+        d = self.call_desc(y_dtype, one_wave_per_unit)
+        _check(_lib.vbq_gemm_small(ctypes.byref(d), ctypes.c_void_p(self.blob.data_ptr()), M,
                                    ctypes.c_void_p(X.data_ptr()), X.stride(0), ctypes.c_void_p(Y.data_ptr()),
                                    Y.stride(0), _stream_handle(stream)), "vbq_gemm_small")
         return Y
@@ -336,12 +412,15 @@ class BucketedMatrix:
         return sum(p[1].nbytes for p in self.parts)
 
     def gemv(self, x, y=None, stream=None):
-        """y[N] (float32) = w_hat @ x: one vbq_gemv_rows per bucket, on one stream."""
+        """y[N] = w_hat @ x: one vbq_gemv_rows per bucket, on one stream; y float32
+        (or a given float16 tensor)."""
         import torch
         dev = self.parts[0][1].blob.device
         if y is None:
             y = torch.empty(self.N, dtype=torch.float32, device=dev)
-        _need(y, "y", torch.float32, self.N, dev)
+        if y.dtype not in (torch.float32, torch.float16):
+            raise ValueError("y must be float32 or float16")
+        _need(y, "y", y.dtype, self.N, dev)
         for _, Wp, rows in self.parts:
             Wp.gemv_rows(x, y, rows, stream)
         return y

@@ -80,7 +80,7 @@ PAIR_GEOMS = [(6144, 4096, 0, 0), (4096, 14336, 0, 0), (1000, 4096, 0, 0), (37, 
 
 
 @pytest.mark.parametrize("N,K,R,C", PAIR_GEOMS)
-def test_pair_kernel_matches_one_wave_per_unit(vbq, N, K, R, C, monkeypatch):
+def test_pair_kernel_matches_one_wave_per_unit(vbq, N, K, R, C):
     """Both kernels match the oracle; where one wave per unit also takes whole
     units (four or more units per tile) the two add the same per-unit row
     sums in the same order, so their outputs are bitwise equal."""
@@ -90,11 +90,8 @@ def test_pair_kernel_matches_one_wave_per_unit(vbq, N, K, R, C, monkeypatch):
     x = synth.make_x(spec, 47)[0]
     Wp = _packed(vbq, q, s, bits, R, C)
     xd = _x_dev(x)
-    monkeypatch.delenv("VBQ_ONE_WAVE_PER_UNIT", raising=False)
     y_pair = Wp.gemv(xd).cpu().numpy()
-    monkeypatch.setenv("VBQ_ONE_WAVE_PER_UNIT", "1")
-    y_one = Wp.gemv(xd).cpu().numpy()
-    monkeypatch.delenv("VBQ_ONE_WAVE_PER_UNIT")
+    y_one = Wp.gemv(xd, one_wave_per_unit=True).cpu().numpy()
     if Wp.desc.n_chunks >= 4:
         assert np.array_equal(y_pair, y_one)
     want, mag = omatmul.gemv(q, s, x), omatmul.row_magnitude(q, s, x)
@@ -104,9 +101,7 @@ def test_pair_kernel_matches_one_wave_per_unit(vbq, N, K, R, C, monkeypatch):
     X = synth.make_x(spec, 47, M=2)
     Xd = torch.from_numpy(np.ascontiguousarray(X)).to("cuda")
     Y_pair = Wp.gemm_small(Xd).cpu().numpy()
-    monkeypatch.setenv("VBQ_ONE_WAVE_PER_UNIT", "1")
-    Y_one = Wp.gemm_small(Xd).cpu().numpy()
-    monkeypatch.delenv("VBQ_ONE_WAVE_PER_UNIT")
+    Y_one = Wp.gemm_small(Xd, one_wave_per_unit=True).cpu().numpy()
     if Wp.desc.n_chunks >= 4:
         assert np.array_equal(Y_pair, Y_one)
     for m in range(2):

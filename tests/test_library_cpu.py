@@ -211,6 +211,79 @@ def test_null_and_buffer_errors():
                         None) == 7
 
 
+def test_call_flags_are_checked_before_any_launch():
+    """Descriptor call options: unknown bits are refused, VBQ_Y_F16 needs only
+    2-byte alignment of y; all of it before anything touches the GPU."""
+    lib = vbq.lib()
+    rng = synth.rng_for(4)
+    bits, q, s = _random_codes(rng, 8, 256)
+    _, d = vbq.pack_codes(q, s, bits)
+    A = 1 << 20  # aligned stand-in addresses, never dereferenced on this path
+    d.flags = 4
+    assert lib.vbq_gemv(ctypes.byref(d), ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_void_p(A), None) == 10
+    assert lib.vbq_gemm_small(ctypes.byref(d), ctypes.c_void_p(A), 3, ctypes.c_void_p(A), 256,
+                              ctypes.c_void_p(A), 8, None) == 10
+    assert lib.vbq_gemv_rows(ctypes.byref(d), ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_void_p(A), 8,
+                             ctypes.c_void_p(A), None) == 10
+    d.flags = 0  # float y must be 4-byte aligned
+    assert lib.vbq_gemv(ctypes.byref(d), ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_void_p(A + 2), None) == 7
+    d.flags = vbq.Y_F16  # fp16 y: 2-byte alignment, an odd address is refused
+    assert lib.vbq_gemv(ctypes.byref(d), ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_void_p(A + 1), None) == 7
+    assert lib.vbq_gemm_small(ctypes.byref(d), ctypes.c_void_p(A), 4, ctypes.c_void_p(A), 256,
+                              ctypes.c_void_p(A + 1), 8, None) == 7
+    d.flags = vbq.Y_F16 | vbq.ONE_WAVE_PER_UNIT
+    assert vbq.desc_check(d) == 0  # the options are not part of the layout
+
+
+def test_pack_row_buckets_c_abi():
+    """vbq_pack_row_buckets: every bucket's bytes are the oracle packer's bytes
+    for that width's rows, at a 256-byte aligned offset; row_index lists the
+    rows bucket by bucket; the size call agrees."""
+    spec = synth.MatrixSpec("h", 0, 4, 513, 768, row_tiers=synth.RECIPE_HEAD_TIERS)
+    bits, q, s = synth.make_matrix(spec, 75)
+    w = bits[:, 0]
+    blob, bk, row_index = vbq.pack_row_buckets_raw(q, s, w, tile_rows=32)
+    assert [b.bits for b in bk] == sorted(set(int(v) for v in w))
+    assert sorted(row_index.tolist()) == list(range(spec.N))
+    end = 0
+    for b in bk:
+        assert b.blob_offset % 256 == 0 and b.blob_offset >= end and b.reserved == 0
+        rows = row_index[b.row_begin:b.row_begin + b.n_rows]
+        assert np.all(np.diff(rows) > 0) and np.all(w[rows] == b.bits) and b.desc.N == b.n_rows
+        ob, _ = olayout.pack(q[rows], s[rows], bits[rows], b.desc.tile_rows, b.desc.chunk_groups)
+        got = np.asarray(blob)[b.blob_offset:b.blob_offset + b.desc.total_bytes]
+        assert np.array_equal(got, np.asarray(ob))
+        end = b.blob_offset + b.desc.total_bytes
+    lib = vbq.lib()
+    nbytes, nb = ctypes.c_size_t(0), ctypes.c_int32(0)
+    wb = np.ascontiguousarray(w)
+    o32 = vbq.VbqPackOpts(32, 0, 0, 0)
+    assert lib.vbq_pack_row_buckets_size(spec.N, spec.K, wb.ctypes.data_as(ctypes.c_void_p), ctypes.byref(o32),
+                                         ctypes.byref(nbytes), ctypes.byref(nb)) == 0
+    assert nb.value == len(bk) and nbytes.value == end
+    # errors: a width outside {1,2,4,8}, NULL, a buffer too small, a level outside its width's set
+    bad = wb.copy()
+    bad[7] = 3
+    assert _status(lambda: vbq.pack_row_buckets_raw(q, s, bad)) == "VBQ_ERR_BITS"
+    assert lib.vbq_pack_row_buckets_size(spec.N, spec.K, None, None, ctypes.byref(nbytes), ctypes.byref(nb)) == 1
+    small = np.zeros(64, dtype=np.uint64)
+    out = (vbq.VbqBucket * vbq.MAX_BUCKETS)()
+    ri = np.zeros(spec.N, dtype=np.int32)
+    assert lib.vbq_pack_row_buckets(spec.N, spec.K, q.ctypes.data_as(ctypes.c_void_p),
+                                    s.ctypes.data_as(ctypes.c_void_p), wb.ctypes.data_as(ctypes.c_void_p), None,
+                                    small.ctypes.data_as(ctypes.c_void_p), small.nbytes, out, ctypes.byref(nb),
+                                    ri.ctypes.data_as(ctypes.c_void_p)) == 7
+    qq = np.array(q)
+    r1 = int(np.nonzero(w == 1)[0][0])
+    qq[r1, 0] = 0  # 1-bit levels are +-1
+    assert _status(lambda: vbq.pack_row_buckets_raw(qq, s, w)) == "VBQ_ERR_CODE_RANGE"
+    # vbq_gemv_buckets: bucket count checked first, none is a no-op
+    assert lib.vbq_gemv_buckets(out, 5, None, None, None, None, 0, None) == 2
+    assert lib.vbq_gemv_buckets(out, -1, None, None, None, None, 0, None) == 2
+    assert lib.vbq_gemv_buckets(out, 0, None, None, None, None, 0, None) == 0
+    assert lib.vbq_gemv_buckets(out, 1, None, None, None, None, 0, None) == 1
+
+
 def test_single_hip_runtime():
     """libvbq must share torch's HIP runtime: one libamdhip64 in the process."""
     assert len(vbq.hip_runtimes()) == 1
