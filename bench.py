@@ -11,10 +11,16 @@ from the {1:.69, 2:.15, 4:.12, 8:.04} mix), 129 GEMVs, ~1.95 GB streamed.
     python bench.py --qat     # the selection-path forward (training), its own JSON line
 
 Prints one JSON line.  `value` is effective GB/s = algorithmic bytes of the
-step / wall time per step (HIP-graph replay of the step).  The roofline block
-times every launch of the GEMV kernel with HIP events recorded on the stream
-it runs on.  cpu_baseline times the double-precision oracle on a bounded
-sample of the same workload (host cores; a baseline only).
+step / wall time per step (HIP-graph replay of the step, or eager launches if
+faster).  `roofline` is the dominant kernel of the step (the one with the most
+GPU time): algorithmic bytes per launch / its average launch duration, timed
+with HIP events on the launch stream around replays of a graph of its launches;
+`traffic` is its HBM bytes per launch from the committed rocprofv3 counter
+summary when that was taken on the current kernel source.  `step_roofline`
+lists every kernel of the step the same way.  The default run also times the
+one-GEMV and 131M-class workloads hot and cold and the device's plain
+streaming-read ceiling.  cpu_baseline times the double-precision oracle on a
+bounded sample of the same workload (host cores; a baseline only).
 """
 
 import argparse
@@ -59,12 +65,10 @@ def kernel_source_hash(sources=None):
     return h.hexdigest()
 
 
-def measured_traffic(config, path=None, expected_config=None, sources=None):
-    """HBM bytes per launch from a committed counter summary, or None when that
-    summary is missing, was taken on another kernel source, or on another
-    configuration than `config`."""
-    path = TRAFFIC_FILE if path is None else path
-    expected_config = TRAFFIC_CONFIG if expected_config is None else expected_config
+def _traffic_fields(config, path, expected_config, sources):
+    """The `- key: value` fields of a committed counter summary, or None when it
+    is missing, was taken on another kernel source, or on another configuration
+    than `config`."""
     if config != expected_config:
         return None
     try:
@@ -75,11 +79,41 @@ def measured_traffic(config, path=None, expected_config=None, sources=None):
                     k, v = line[2:].split(":", 1)
                     v = v.strip()
                     fields[k.strip()] = v.split("`")[1] if v.startswith("`") else v
-        if fields.get("kernel_source_sha256") != kernel_source_hash(sources) or fields.get("config") != expected_config:
-            return None
-        return int(fields["hbm_bytes_per_launch"])
-    except (OSError, KeyError, ValueError):
+    except OSError:
         return None
+    if fields.get("kernel_source_sha256") != kernel_source_hash(sources) or fields.get("config") != expected_config:
+        return None
+    return fields
+
+
+def measured_traffic(config, path=None, expected_config=None, sources=None):
+    """HBM bytes per launch (every launch of the run) from a committed counter
+    summary, or None (see _traffic_fields)."""
+    path = TRAFFIC_FILE if path is None else path
+    expected_config = TRAFFIC_CONFIG if expected_config is None else expected_config
+    fields = _traffic_fields(config, path, expected_config, sources)
+    try:
+        return None if fields is None else int(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def measured_traffic_per_kernel(config, path=None):
+    """{kernel name: HBM bytes per launch} from the committed counter summary of
+    the decode step, or None (see _traffic_fields)."""
+    fields = _traffic_fields(config, TRAFFIC_FILE if path is None else path, TRAFFIC_CONFIG, None)
+    try:
+        return None if fields is None else {k: int(v["hbm_bytes_per_launch"])
+                                            for k, v in json.loads(fields["per_kernel"]).items()}
+    except (KeyError, ValueError, TypeError):
+        return None
+
+
+def canonical_kernel(name):
+    """A profiler's kernel name in vbq_kernel_name's form: template arguments
+    without spaces, the default last argument of vbq_mv_kernel dropped."""
+    n = name.replace("void ", "").replace("(anonymous namespace)::", "").split("(")[0].replace(" ", "")
+    return n[:-4] + ">" if n.endswith(",-1>") else n
 
 
 def pmc_summary(fetch_dir, write_dir, kernel="vbq_mv_", sources=None):
@@ -90,7 +124,7 @@ def pmc_summary(fetch_dir, write_dir, kernel="vbq_mv_", sources=None):
     import csv
     import glob
 
-    def per_kernel(d, counter):
+    def per_kernel(d, counter, by_name=False):
         path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
         acc = {}
         for r in csv.DictReader(open(path)):
@@ -98,7 +132,8 @@ def pmc_summary(fetch_dir, write_dir, kernel="vbq_mv_", sources=None):
                 continue
             name = r["Kernel_Name"]
             # e.g. every one-row GEMV kernel of the decode step (per-unit and two-waves-per-unit)
-            key = "vbq" if kernel in name else ("copy" if "MulFunctor" in name else None)
+            key = ("vbq" if not by_name else canonical_kernel(name)) if kernel in name else \
+                ("copy" if "MulFunctor" in name and not by_name else None)
             if key is None:
                 continue
             acc.setdefault(key, {}).setdefault(r["Dispatch_Id"], 0.0)
@@ -112,11 +147,17 @@ def pmc_summary(fetch_dir, write_dir, kernel="vbq_mv_", sources=None):
     fv, wv = np.array(f["vbq"]), np.array(w["vbq"])
     fetch_b = float(np.mean(fv)) * f_scale * 1024
     write_b = float(np.mean(wv)) * w_scale * 1024
+    per = {}
+    fk, wk = per_kernel(fetch_dir, "FETCH_SIZE", by_name=True), per_kernel(write_dir, "WRITE_SIZE", by_name=True)
+    for name in sorted(fk):
+        if name in wk:
+            b = float(np.mean(fk[name])) * f_scale * 1024 + float(np.mean(wk[name])) * w_scale * 1024
+            per[name] = {"launches": len(fk[name]), "hbm_bytes_per_launch": int(round(b))}
     return {"launches": int(fv.size), "fetch_kib_per_launch_raw": float(np.mean(fv)),
             "write_kib_per_launch_raw": float(np.mean(wv)), "copy_fetch_kib": f_copy, "copy_write_kib": w_copy,
             "fetch_scale": f_scale, "write_scale": w_scale, "fetch_bytes_per_launch": fetch_b,
             "write_bytes_per_launch": write_b, "hbm_bytes_per_launch": int(round(fetch_b + write_b)),
-            "kernel_source_sha256": kernel_source_hash(sources)}
+            "per_kernel": per, "kernel_source_sha256": kernel_source_hash(sources)}
 
 
 def log(msg):
@@ -208,7 +249,7 @@ def write_traffic_file(path, summ):
     lines = [
         "# HBM traffic of vbq_mv_kernel<1>: 9B-class decode step (129 GEMVs, M=1)",
         "",
-        "Two counter passes over `bench.py --profile --steps 2 --warmup 1` (3 steps x 129 launches),",
+        "Two counter passes over `bench.py --profile --steps 2 --warmup 1` (the step's HIP graph replayed 3 times),",
         "then a plain copy of 256 MiB (torch.mul by 1.0) to scale the counters to bytes:",
         "",
         "```",
@@ -233,6 +274,7 @@ def write_traffic_file(path, summ):
         f"- fetch_bytes_per_launch: {summ['fetch_bytes_per_launch']:.0f}",
         f"- write_bytes_per_launch: {summ['write_bytes_per_launch']:.0f}",
         f"- hbm_bytes_per_launch: {summ['hbm_bytes_per_launch']}",
+        f"- per_kernel: `{json.dumps(summ.get('per_kernel', {}), sort_keys=True)}`",
         f"- kernel_source_sha256: `{summ['kernel_source_sha256']}` (vbq_kernels.hip, vbq_layout.hpp, "
         "vbq_pack.cpp)",
         "",
@@ -489,10 +531,13 @@ def main():
     ap.add_argument("--workers", type=int, default=min(12, len(os.sched_getaffinity(0))))
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-small", action="store_true",
+                    help="skip the hot / cold timing of workloads 0 and 1 that the default run adds")
     ap.add_argument("--cold", type=int, default=0, metavar="K",
                     help="also time K steps one by one, each after a 1 GiB write that evicts L2 and the "
                          "Infinity Cache (the write is outside the timed region)")
-    ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 (eager launches only)")
+    ap.add_argument("--profile", action="store_true",
+                    help="short run for rocprofv3: the step's graph replayed --steps times, then a calibration copy")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs of --profile (FETCH_SIZE, WRITE_SIZE) and exit")
     ap.add_argument("--write-traffic", metavar="PATH", help="with --pmc-summary: write the traffic summary file")
@@ -521,238 +566,107 @@ def main():
     wl, packed = prepare(args.workload, args.workers, args.uniform, args.recipe)
 
     import torch
-    from paper_2607_02893_amd import synth, vbq
+    from paper_2607_02893_amd import vbq
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    mats = []         # per matrix: ([(PackedMatrix, output rows or None)], x, y, algorithmic bytes)
-    launch_args = []  # per launch: (desc, blob, x, y, output-row map or 0, len(y))
-    launch_alg = []
-    total_alg, total_w, blob_bytes = 0.0, 0, 0
-    for idx, parts, nw in packed:
-        spec = wl.matrices[idx]
-        xm = synth.make_x(spec, wl.seed, args.batch)
-        x = torch.from_numpy(np.ascontiguousarray(xm[0] if args.batch == 1 else xm)).to(dev)
-        y = torch.empty(spec.N if args.batch == 1 else (args.batch, spec.N), dtype=torch.float32, device=dev)
-        dev_parts, alg = [], 0.0
-        for rows, blob, dbytes, palg in parts:
-            desc = vbq.VbqDesc.from_buffer_copy(dbytes)
-            Wp = vbq.PackedMatrix(blob, desc, device=dev)
-            rt = None if rows is None else torch.from_numpy(rows).to(dev)
-            dev_parts.append((Wp, rt))
-            palg += (2 * spec.K + 4 * desc.N) * (args.batch - 1)  # x and y of the extra rows
-            launch_args.append((desc, Wp.blob.data_ptr(), x.data_ptr(), y.data_ptr(),
-                                0 if rt is None else rt.data_ptr(), spec.N))
-            launch_alg.append(palg)
-            alg += palg
-            blob_bytes += desc.total_bytes
-        mats.append((dev_parts, x, y, alg))
-        total_alg += alg
-        total_w += nw
-    del packed
     stream = torch.cuda.current_stream()
-    sptr = stream.cuda_stream
     M = args.batch
-
-    def launch(d, b, x, y, rows, ylen, stream_ptr):
-        if rows:
-            return vbq.raw_gemv_rows(d, b, x, y, ylen, rows, stream_ptr)
-        if M == 1:
-            return vbq.raw_gemv(d, b, x, y, stream_ptr)
-        return vbq.raw_gemm_small(d, b, M, x, d.K, y, d.N, stream_ptr)
-
-    def step():
-        for la in launch_args:
-            st = launch(*la, sptr)
-            if st != 0:
-                raise vbq.VbqError(st, "vbq_gemv / vbq_gemv_rows / vbq_gemm_small")
-
-    log(f"{len(mats)} matrices in {len(launch_args)} launches, {total_w / 1e9:.2f}G weights, "
-        f"algorithmic {total_alg / 1e6:.1f} MB/step, "
-        f"blobs {blob_bytes / 1e6:.1f} MB")
+    st = build_step(wl, packed, M, dev)
+    del packed
+    log(f"{len(st.mats)} matrices in {len(st.launch_args)} launches, {st.total_w / 1e9:.2f}G weights, "
+        f"algorithmic {st.total_alg / 1e6:.1f} MB/step, blobs {st.blob_bytes / 1e6:.1f} MB")
     for _ in range(args.warmup):
-        step()
+        st.run(stream.cuda_stream)
     torch.cuda.synchronize()
+    g = st.graph(stream)
 
     if args.profile:
+        # the timed loop itself (graph replay) for the profiler, then the
+        # calibration copy of known size for the HBM byte counters
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(args.steps):
-            step()
+            g.replay()
         torch.cuda.synchronize()
         dt = (time.perf_counter() - t0) / args.steps
-        log(f"profile run: {args.steps} eager steps, {1e6 * dt:.1f} us/step")
-        # calibration: a plain copy of known size for the HBM byte counters
+        log(f"profile run: {args.steps} graph replays, {1e6 * dt:.1f} us/step")
         src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
             torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
-        print(json.dumps({"profile_run": True, "us_per_step_eager": round(1e6 * dt, 2)}), flush=True)
+        print(json.dumps({"profile_run": True, "us_per_step_graph": round(1e6 * dt, 2)}), flush=True)
         return
 
-    def timed(run, n):
-        """Wall time per step (host clock, synchronized on both sides) and GPU
-        time per step (HIP events recorded on the launch stream around the
-        same region)."""
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        e0.record(stream)
-        for _ in range(n):
-            run()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t0) / n, e0.elapsed_time(e1) * 1e-3 / n
-
-    # eager timing
-    eager_s, eager_gpu_s = timed(step, args.steps)
+    # eager launches and graph replay of the same launches; the faster is reported
+    eager_s, eager_gpu_s = timed(lambda: st.run(stream.cuda_stream), args.steps, stream)
     log(f"eager: {1e6 * eager_s:.1f} us/step (events {1e6 * eager_gpu_s:.1f})")
-
-    # graph timing (same launches captured once, replayed on the same stream)
-    graph_s = graph_gpu_s = None
-    try:
-        g = torch.cuda.CUDAGraph()
-        cap = torch.cuda.Stream()
-        cap.wait_stream(stream)
-        with torch.cuda.stream(cap):
-            csp = cap.cuda_stream
-            g.capture_begin()
-            for la in launch_args:
-                st = launch(*la, csp)
-                if st != 0:
-                    raise vbq.VbqError(st, "vbq_gemv (capture)")
-            g.capture_end()
-        stream.wait_stream(cap)
-        for _ in range(args.warmup):
-            g.replay()
-        graph_s, graph_gpu_s = timed(g.replay, args.steps)
-        log(f"graph: {1e6 * graph_s:.1f} us/step (events {1e6 * graph_gpu_s:.1f})")
-        # graph result equals eager result
-        ref = [m[2].clone() for m in mats[:3] + mats[-1:]]
-        step()
-        torch.cuda.synchronize()
-        for r, m in zip(ref, mats[:3] + mats[-1:]):
-            assert torch.equal(r, m[2]), "graph replay differs from eager launch"
-    except Exception as e:  # graph capture is an optimisation of the same launches
-        log(f"graph capture unavailable: {e}")
-
-    # the distribution of single steps (each bracketed by its own events; the
-    # timed region above gives the mean)
-    run_one = g.replay if graph_s is not None and graph_s <= eager_s else step
-    n_dist = min(100, args.steps)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_dist)]
-    for e0, e1 in ev:
-        e0.record(stream)
-        run_one()
-        e1.record(stream)
+    for _ in range(args.warmup):
+        g.replay()
+    graph_s, graph_gpu_s = timed(g.replay, args.steps, stream)
+    log(f"graph: {1e6 * graph_s:.1f} us/step (events {1e6 * graph_gpu_s:.1f})")
+    ref = [m[2].clone() for m in st.mats[:3] + st.mats[-1:]]
+    st.run(stream.cuda_stream)
     torch.cuda.synchronize()
-    st_us = np.array([e0.elapsed_time(e1) * 1e3 for e0, e1 in ev])
-    step_dist = {"median": round(float(np.median(st_us)), 2), "p10": round(float(np.percentile(st_us, 10)), 2),
-                 "p90": round(float(np.percentile(st_us, 90)), 2), "steps": n_dist,
-                 "timing": "HIP events around each step, on the launch stream"}
+    for r, m in zip(ref, st.mats[:3] + st.mats[-1:]):
+        assert torch.equal(r, m[2]), "graph replay differs from eager launch"
+    use_graph = graph_s <= eager_s
+    wall_s = graph_s if use_graph else eager_s
+    run_one = g.replay if use_graph else (lambda: st.run(stream.cuda_stream))
+    step_dist = distribution(run_one, min(100, args.steps), stream)
     log(f"single steps: median {step_dist['median']} us, p10 {step_dist['p10']}, p90 {step_dist['p90']}")
 
-    # cold steps: every byte of the step comes from HBM (small workloads
-    # otherwise stay resident in the 256 MB Infinity Cache between steps)
-    cold_us = None
-    if args.cold > 0:
-        flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
-        run1 = g.replay if graph_s is not None else step
-        ts = []
-        for _ in range(args.cold):
-            flush.fill_(1.0)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            run1()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1) * 1e3)
-        del flush
-        torch.cuda.empty_cache()
-        cold_us = {"median": round(float(np.median(ts)), 2), "p10": round(float(np.percentile(ts, 10)), 2),
-                   "p90": round(float(np.percentile(ts, 90)), 2), "steps": args.cold}
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB: evicts L2 and the Infinity Cache
+    cold_us = cold_steps(run_one, args.cold, flush, stream) if args.cold > 0 else None
+    if cold_us:
         log(f"cold: {cold_us['median']:.1f} us/step (median of {args.cold}, caches flushed before each)")
 
-    # the faster of the two timings of the same launches (a graph of one small
-    # kernel is bound by the graph launch itself)
-    use_graph = graph_s is not None and graph_s <= eager_s
-    wall_s = graph_s if use_graph else eager_s
-    gpu_s = graph_gpu_s if use_graph else eager_gpu_s
-    # Every launch of the step is the same kernel and they run back to back,
-    # so its average launch duration is the step's GPU time / launches.
-    n_launch = len(launch_args)
-    per_launch_s = gpu_s / n_launch
-    alg_per_launch = total_alg / n_launch
-    achieved = alg_per_launch / per_launch_s / 1e9
-
-    # per-matrix breakdown (diagnostic; each launch bracketed by its own events)
-    n_ev = min(5, args.steps)
-    starts = [[torch.cuda.Event(enable_timing=True) for _ in launch_args] for _ in range(n_ev)]
-    ends = [[torch.cuda.Event(enable_timing=True) for _ in launch_args] for _ in range(n_ev)]
-    for r in range(n_ev):
-        for i, la in enumerate(launch_args):
-            starts[r][i].record(stream)
-            launch(*la, sptr)
-            ends[r][i].record(stream)
-    torch.cuda.synchronize()
-    dur = np.median(np.array([[starts[r][i].elapsed_time(ends[r][i]) * 1e-3 for i in range(n_launch)]
-                              for r in range(n_ev)]), axis=0)
-    per_shape = {}
-    for i, la in enumerate(launch_args):
-        key = f"{la[0].N}x{la[0].K}" + (" (row bucket)" if la[4] else "")
-        e = per_shape.setdefault(key, {"count": 0, "us": [], "alg_bytes": launch_alg[i]})
-        e["count"] += 1
-        e["us"].append(1e6 * dur[i])
-    per_shape = {k: {"count": v["count"], "us_median": round(float(np.median(v["us"])), 2),
-                     "GBps": round(v["alg_bytes"] / (1e-6 * float(np.median(v["us"]))) / 1e9, 1)}
-                 for k, v in per_shape.items()}
+    # every kernel of the step alone: its launches, in step order, as one graph
+    # replayed back to back on the launch stream (HIP events around the loop)
+    kern = per_kernel_timing(st, stream, args.steps, args.warmup)
+    dominant = max(kern, key=lambda k: kern[k]["launches"] * kern[k]["avg_launch_us"])
+    sum_kernel_us = sum(v["launches"] * v["avg_launch_us"] for v in kern.values())
+    log("kernels: " + ", ".join(f"{k} x{v['launches']} {v['avg_launch_us']:.2f} us {v['GBps']:.0f} GB/s"
+                                for k, v in kern.items()))
+    per_shape = per_shape_timing(st, stream, min(5, args.steps))
     log(f"per shape (launch bracketed by events): {per_shape}")
 
-    # dense fp16 baseline on the dequantized weights (context: the paper's FP16 comparison)
-    dense = None
-    if not args.no_dense:
-        try:
-            ws = []
-            for parts, x, y, _ in mats:
-                if parts[0][1] is None:
-                    ws.append(parts[0][0].dequant().half())
-                else:  # row buckets: scatter each bucket's rows back into place
-                    w = torch.empty((y.shape[-1], parts[0][0].K), dtype=torch.float16, device=dev)
-                    for Wp, rows in parts:
-                        w[rows.long()] = Wp.dequant().half()
-                    ws.append(w)
-            torch.cuda.synchronize()
-            xs = [m[1].view(M, -1) for m in mats]
+    dense = None if args.no_dense else dense_baseline(st, M, args.steps, dev, min(eager_s, graph_s))
+    if dense:
+        log(f"dense fp16: {dense['us_per_step']:.1f} us/step")
 
-            def dense_step():
-                for w, xx in zip(ws, xs):
-                    torch.nn.functional.linear(xx, w)
-            for _ in range(3):
-                dense_step()
-            torch.cuda.synchronize()
-            nd = max(5, args.steps // 10)
-            t0 = time.perf_counter()
-            for _ in range(nd):
-                dense_step()
-            torch.cuda.synchronize()
-            dense_s = (time.perf_counter() - t0) / nd
-            dense = {"us_per_step": round(1e6 * dense_s, 1), "weight_bytes": 2 * total_w,
-                     "speedup_vbq": round(dense_s / min(eager_s, graph_s or eager_s), 2),
-                     "note": "torch F.linear (fp16) over the dequantized weights, eager launches"}
-            del ws
-            torch.cuda.empty_cache()
-            log(f"dense fp16: {1e6 * dense_s:.1f} us/step")
-        except Exception as e:
-            log(f"dense baseline skipped: {e}")
+    config_key = (f"workload {args.workload}, M {M}, "
+                  f"widths {'recipe' if args.recipe else 'uniform ' + str(args.uniform) if args.uniform else 'mixed'}")
+    traffic_all = measured_traffic(config_key)
+    traffic_k = measured_traffic_per_kernel(config_key)
+    dk = kern[dominant]
+    t_dom = traffic_k.get(dominant) if traffic_k else None
+    achieved = dk["alg_bytes_per_launch"] / (1e-6 * dk["avg_launch_us"]) / 1e9
+    value = st.total_alg / wall_s / 1e9
+    step_counters = None
+    if traffic_k and all(k in traffic_k for k in kern):
+        hbm = sum(traffic_k[k] * v["launches"] for k, v in kern.items())
+        step_counters = {"hbm_bytes_per_step": hbm, "vs_algorithmic": round(hbm / st.total_alg, 3),
+                         "frac_of_sum_kernel_time": round(hbm / (1e-6 * sum_kernel_us) / 1e9 / PEAK_HBM_GBS, 4),
+                         "frac_of_step_time": round(hbm / wall_s / 1e9 / PEAK_HBM_GBS, 4)}
 
-    traffic = measured_traffic(f"workload {args.workload}, M {M}, "
-                               f"widths {'recipe' if args.recipe else 'uniform ' + str(args.uniform) if args.uniform else 'mixed'}")
-    value = total_alg / wall_s / 1e9
+    small = None
+    if not args.no_small and args.workload == 3 and M == 1 and not args.recipe and not args.uniform:
+        small = {f"workload {c}": small_workload(c, args, dev, stream, flush) for c in (0, 1)}
+    ceiling = read_ceiling(flush, stream)
+    log(f"streaming-read ceiling: {ceiling['GBps']:.0f} GB/s ({ceiling['blocks']} blocks)")
+    del flush
+    torch.cuda.empty_cache()
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(wl)
         log(f"cpu oracle: {cpu['value']} ms/step ({cpu['sample']})")
+    n_launch = len(st.launch_args)
     out = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -767,34 +681,300 @@ def main():
         "dtype": "f32",
         "precision": "fp16 activations x {1,2,4,8}-bit codes with fp16 group scales, fp32 accumulation",
         "data": "synthetic (seeded draws; no trained weights)",
-        "config": {"workload": f"{wl.name} decode step (workload {args.workload}): {len(mats)} GEMVs"
-                               f"{f' in {n_launch} launches' if n_launch != len(mats) else ''}, "
-                               f"{total_w / 1e9:.2f}G weights", "M": M,
+        "config": {"workload": f"{wl.name} decode step (workload {args.workload}): {len(st.mats)} GEMVs"
+                               f"{f' in {n_launch} launches' if n_launch != len(st.mats) else ''}, "
+                               f"{st.total_w / 1e9:.2f}G weights", "M": M,
                    "uniform_bits": args.uniform or None, "recipe": bool(args.recipe),
-                   "algorithmic_bytes_per_step": int(total_alg), "blob_bytes": int(blob_bytes),
+                   "algorithmic_bytes_per_step": int(st.total_alg), "blob_bytes": int(st.blob_bytes),
                    "timing": "HIP-graph replay of the step" if use_graph else "eager launches"},
         "us_per_step": round(1e6 * wall_s, 2),
         "us_per_step_eager": round(1e6 * eager_s, 2),
-        "us_per_step_graph": round(1e6 * graph_s, 2) if graph_s is not None else None,
+        "us_per_step_graph": round(1e6 * graph_s, 2),
         "us_per_step_cold": cold_us,
         "us_per_step_distribution": step_dist,
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                     "kernel": ("vbq_mv_kernel<1, NW, width class> (one width; LM head as row buckets)" if args.recipe
-                                else "vbq_mv_kernel<1> / vbq_mv_pair_kernel (one-row GEMV)" if M == 1 else
-                                "vbq_mv_kernel<2>" if M == 2 else "vbq_mm_kernel"),
-                     "launches_per_step": n_launch,
-                     "algorithmic_bytes_per_launch": round(alg_per_launch),
-                     "avg_launch_us": round(1e6 * per_launch_s, 3),
-                     "timing": "HIP events on the launch stream around the timed region / launches",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": t_dom,
+                     "kernel": dominant,
+                     "launches_per_step": dk["launches"],
+                     "share_of_step_kernel_time": round(dk["launches"] * dk["avg_launch_us"] / sum_kernel_us, 3),
+                     "algorithmic_bytes_per_launch": round(dk["alg_bytes_per_launch"]),
+                     "avg_launch_us": dk["avg_launch_us"],
+                     "timing": "HIP events on the launch stream around K replays of a graph of this kernel's "
+                               "launches of one step (step order, back to back)",
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                     "traffic_vs_algorithmic": round(traffic / alg_per_launch, 3) if traffic else None},
+                     "traffic_vs_algorithmic": round(t_dom / dk["alg_bytes_per_launch"], 3) if t_dom else None,
+                     "frac_from_counters": round(t_dom / (1e-6 * dk["avg_launch_us"]) / 1e9 / PEAK_HBM_GBS, 4)
+                     if t_dom else None},
+        "step_roofline": {"sum_kernel_us": round(sum_kernel_us, 1),
+                          "frac_algorithmic_of_step_time": round(value / PEAK_HBM_GBS, 4),
+                          "frac_algorithmic_of_sum_kernel_time":
+                              round(st.total_alg / (1e-6 * sum_kernel_us) / 1e9 / PEAK_HBM_GBS, 4),
+                          "counters": step_counters,
+                          "traffic_all_launches_per_launch": traffic_all,
+                          "kernels": kern},
+        "read_ceiling": ceiling,
+        "small_workloads": small,
         "per_shape": per_shape,
         "cpu_baseline": cpu,
         "dense_fp16_baseline": dense,
     }
     print(json.dumps(out), flush=True)
+
+
+class Step:
+    """The launches of one decode step on device: per launch (desc, blob, x, y,
+    output-row map or 0, len(y)), its algorithmic bytes and kernel name."""
+
+    def __init__(self, M):
+        self.M = M
+        self.mats = []        # per matrix: ([(PackedMatrix, rows or None)], x, y, algorithmic bytes)
+        self.launch_args = []
+        self.launch_alg = []
+        self.kernels = []
+        self.total_alg = 0.0
+        self.total_w = 0
+        self.blob_bytes = 0
+
+    def launch(self, i, stream_ptr):
+        from paper_2607_02893_amd import vbq
+        d, b, x, y, rows, ylen = self.launch_args[i]
+        if rows:
+            return vbq.raw_gemv_rows(d, b, x, y, ylen, rows, stream_ptr)
+        if self.M == 1:
+            return vbq.raw_gemv(d, b, x, y, stream_ptr)
+        return vbq.raw_gemm_small(d, b, self.M, x, d.K, y, d.N, stream_ptr)
+
+    def run(self, stream_ptr, idx=None):
+        from paper_2607_02893_amd import vbq
+        for i in (range(len(self.launch_args)) if idx is None else idx):
+            r = self.launch(i, stream_ptr)
+            if r != 0:
+                raise vbq.VbqError(r, "vbq_gemv / vbq_gemv_rows / vbq_gemm_small")
+
+    def graph(self, stream, idx=None, reps=1):
+        """The launches (all, or those in idx) captured as one HIP graph, reps
+        times in a row (a graph of a few short kernels replayed back to back
+        would otherwise time the host's graph launches)."""
+        import torch
+        g = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        with torch.cuda.stream(cap):
+            g.capture_begin()
+            for _ in range(reps):
+                self.run(cap.cuda_stream, idx)
+            g.capture_end()
+        stream.wait_stream(cap)
+        return g
+
+
+def build_step(wl, packed, M, dev):
+    import torch
+    from paper_2607_02893_amd import synth, vbq
+    st = Step(M)
+    for idx, parts, nw in packed:
+        spec = wl.matrices[idx]
+        xm = synth.make_x(spec, wl.seed, M)
+        x = torch.from_numpy(np.ascontiguousarray(xm[0] if M == 1 else xm)).to(dev)
+        y = torch.empty(spec.N if M == 1 else (M, spec.N), dtype=torch.float32, device=dev)
+        dev_parts, alg = [], 0.0
+        for rows, blob, dbytes, palg in parts:
+            desc = vbq.VbqDesc.from_buffer_copy(dbytes)
+            Wp = vbq.PackedMatrix(blob, desc, device=dev)
+            rt = None if rows is None else torch.from_numpy(rows).to(dev)
+            dev_parts.append((Wp, rt))
+            palg += (2 * spec.K + 4 * desc.N) * (M - 1)  # x and y of the extra rows
+            st.launch_args.append((desc, Wp.blob.data_ptr(), x.data_ptr(), y.data_ptr(),
+                                   0 if rt is None else rt.data_ptr(), spec.N))
+            st.launch_alg.append(palg)
+            st.kernels.append(vbq.kernel_name(desc, M))
+            alg += palg
+            st.blob_bytes += desc.total_bytes
+        st.mats.append((dev_parts, x, y, alg))
+        st.total_alg += alg
+        st.total_w += nw
+    return st
+
+
+def timed(run, n, stream):
+    """Wall time per call (host clock, synchronized on both sides) and GPU time
+    per call (HIP events recorded on the launch stream around the same region)."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(n):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / n, e0.elapsed_time(e1) * 1e-3 / n
+
+
+def distribution(run, n, stream):
+    """Median / p10 / p90 of single calls, each bracketed by its own events."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        run()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    us = np.array([e0.elapsed_time(e1) * 1e3 for e0, e1 in ev])
+    return {"median": round(float(np.median(us)), 2), "p10": round(float(np.percentile(us, 10)), 2),
+            "p90": round(float(np.percentile(us, 90)), 2), "steps": n,
+            "timing": "HIP events around each step, on the launch stream"}
+
+
+def cold_steps(run, n, flush, stream):
+    """Steps timed one by one, each after a 1 GiB write that evicts L2 and the
+    Infinity Cache (the write is outside the timed region)."""
+    import torch
+    ts = []
+    for _ in range(n):
+        flush.fill_(1.0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e3)
+    return {"median": round(float(np.median(ts)), 2), "p10": round(float(np.percentile(ts, 10)), 2),
+            "p90": round(float(np.percentile(ts, 90)), 2), "steps": n,
+            "timing": "HIP events around each step after a 1 GiB flush write"}
+
+
+def per_kernel_timing(st, stream, steps, warmup):
+    """Per kernel of the step: its launches (step order, repeated up to at least
+    64) as one graph, replayed back to back; average launch duration from HIP
+    events around the loop."""
+    out = {}
+    for name in dict.fromkeys(st.kernels):
+        idx = [i for i, k in enumerate(st.kernels) if k == name]
+        reps = -(-64 // len(idx))  # at least 64 launches per replay
+        g = st.graph(stream, idx, reps)
+        for _ in range(max(2, warmup)):
+            g.replay()
+        _, gpu_s = timed(g.replay, max(5, steps // reps), stream)
+        avg = gpu_s / (len(idx) * reps)
+        alg = float(np.mean([st.launch_alg[i] for i in idx]))
+        out[name] = {"launches": len(idx), "avg_launch_us": round(1e6 * avg, 3),
+                     "alg_bytes_per_launch": round(alg), "GBps": round(alg / avg / 1e9, 1)}
+    return out
+
+
+def per_shape_timing(st, stream, n_ev):
+    """Diagnostic: each launch bracketed by its own events (adds event overhead)."""
+    import torch
+    n = len(st.launch_args)
+    starts = [[torch.cuda.Event(enable_timing=True) for _ in range(n)] for _ in range(n_ev)]
+    ends = [[torch.cuda.Event(enable_timing=True) for _ in range(n)] for _ in range(n_ev)]
+    for r in range(n_ev):
+        for i in range(n):
+            starts[r][i].record(stream)
+            st.launch(i, stream.cuda_stream)
+            ends[r][i].record(stream)
+    torch.cuda.synchronize()
+    dur = np.median(np.array([[starts[r][i].elapsed_time(ends[r][i]) * 1e-3 for i in range(n)]
+                              for r in range(n_ev)]), axis=0)
+    per = {}
+    for i, la in enumerate(st.launch_args):
+        key = f"{la[0].N}x{la[0].K}" + (" (row bucket)" if la[4] else "")
+        e = per.setdefault(key, {"count": 0, "us": [], "alg_bytes": st.launch_alg[i], "kernel": st.kernels[i]})
+        e["count"] += 1
+        e["us"].append(1e6 * dur[i])
+    return {k: {"count": v["count"], "kernel": v["kernel"], "us_median": round(float(np.median(v["us"])), 2),
+                "GBps": round(v["alg_bytes"] / (1e-6 * float(np.median(v["us"]))) / 1e9, 1)}
+            for k, v in per.items()}
+
+
+def dense_baseline(st, M, steps, dev, vbq_s):
+    """Dense fp16 F.linear over the dequantized weights (context: the paper's
+    FP16 comparison), eager launches."""
+    import torch
+    try:
+        ws = []
+        for parts, x, y, _ in st.mats:
+            if parts[0][1] is None:
+                ws.append(parts[0][0].dequant().half())
+            else:  # row buckets: scatter each bucket's rows back into place
+                w = torch.empty((y.shape[-1], parts[0][0].K), dtype=torch.float16, device=dev)
+                for Wp, rows in parts:
+                    w[rows.long()] = Wp.dequant().half()
+                ws.append(w)
+        torch.cuda.synchronize()
+        xs = [m[1].view(M, -1) for m in st.mats]
+
+        def dense_step():
+            for w, xx in zip(ws, xs):
+                torch.nn.functional.linear(xx, w)
+        for _ in range(3):
+            dense_step()
+        torch.cuda.synchronize()
+        nd = max(5, steps // 10)
+        t0 = time.perf_counter()
+        for _ in range(nd):
+            dense_step()
+        torch.cuda.synchronize()
+        dense_s = (time.perf_counter() - t0) / nd
+        del ws
+        torch.cuda.empty_cache()
+        return {"us_per_step": round(1e6 * dense_s, 1), "weight_bytes": 2 * st.total_w,
+                "speedup_vbq": round(dense_s / vbq_s, 2),
+                "note": "torch F.linear (fp16) over the dequantized weights, eager launches"}
+    except Exception as e:
+        log(f"dense baseline skipped: {e}")
+        return None
+
+
+def small_workload(cfg, args, dev, stream, flush):
+    """A small decode workload (one GEMV, or the 131M-class step) timed hot
+    (graph replays back to back, weights resident in the caches) and cold
+    (each step after a 1 GiB flush write)."""
+    wl, packed = prepare(cfg, args.workers)
+    st = build_step(wl, packed, 1, dev)
+    g = st.graph(stream)
+    reps = -(-512 // len(st.launch_args))  # hot: the step repeated in one graph, >= 512 launches
+    gr = st.graph(stream, reps=reps)
+    for _ in range(max(5, args.warmup)):
+        gr.replay()
+    _, hot_gpu = timed(gr.replay, max(10, args.steps // reps), stream)
+    hot_gpu /= reps
+    cold = cold_steps(g.replay, max(20, min(100, args.steps)), flush, stream)
+    out = {"name": wl.name, "launches": len(st.launch_args), "algorithmic_bytes": int(st.total_alg),
+           "hot_us": round(1e6 * hot_gpu, 2),
+           "hot_timing": f"HIP events around replays of a graph holding the step {reps} times in a row",
+           "cold_us": cold,
+           "hot_GBps": round(st.total_alg / hot_gpu / 1e9, 1),
+           "cold_GBps": round(st.total_alg / (1e-6 * cold["median"]) / 1e9, 1),
+           "kernels": sorted(set(st.kernels))}
+    log(f"workload {cfg} ({wl.name}): hot {out['hot_us']} us, cold median {cold['median']} us")
+    return out
+
+
+def read_ceiling(buf, stream, reps=10):
+    """The device's plain streaming-read rate (vbq_read_ceiling over a 1 GiB
+    buffer), best over a few grid sizes."""
+    import torch
+    from paper_2607_02893_amd import vbq
+    nbytes = buf.numel() * buf.element_size()
+    best = None
+    for blocks in (4096, 8192, 16384, 32768, 65536, 131072):
+        sink = torch.empty(4 * blocks, dtype=torch.int32, device=buf.device)  # 4 words per block
+
+        def rd():
+            r = vbq.raw_read_ceiling(buf.data_ptr(), nbytes, blocks, sink.data_ptr(), stream.cuda_stream)
+            if r != 0:
+                raise vbq.VbqError(r, "vbq_read_ceiling")
+        rd()
+        _, s = timed(rd, reps, stream)
+        gbs = nbytes / s / 1e9
+        if best is None or gbs > best["GBps"]:
+            best = {"GBps": round(gbs, 1), "blocks": blocks, "bytes": nbytes, "us": round(1e6 * s, 1),
+                    "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4),
+                    "timing": f"HIP events around {reps} back-to-back reads of the buffer"}
+    return best
 
 
 if __name__ == "__main__":

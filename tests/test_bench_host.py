@@ -41,6 +41,9 @@ def test_pmc_summary_scales_by_the_calibration_copy(tmp_path):
     assert s["fetch_bytes_per_launch"] == pytest.approx(2.0 * 200.0 * 1024)
     assert s["write_bytes_per_launch"] == pytest.approx(5.0 * 1024)
     assert s["hbm_bytes_per_launch"] == round(2.0 * 200.0 * 1024 + 5.0 * 1024)
+    assert s["per_kernel"] == {"vbq_mv_kernel<1>": {"launches": 1, "hbm_bytes_per_launch": round(2.0 * 150 * 1024 + 4 * 1024)},
+                               "vbq_mv_pair_kernel<8>": {"launches": 1,
+                                                         "hbm_bytes_per_launch": round(2.0 * 250 * 1024 + 6 * 1024)}}
     q = bench.pmc_summary(str(tmp_path / "f"), str(tmp_path / "w"), kernel="other_kernel", sources=bench.QAT_SOURCES)
     assert q["launches"] == 1 and q["kernel_source_sha256"] == bench.kernel_source_hash(bench.QAT_SOURCES)
 
@@ -50,9 +53,11 @@ def test_traffic_file_is_gated_by_hash_and_config(tmp_path, monkeypatch):
             "copy_write_kib": 1.0, "fetch_scale": 2.0, "write_scale": 1.0, "fetch_bytes_per_launch": 10.0,
             "write_bytes_per_launch": 5.0, "hbm_bytes_per_launch": 15, "kernel_source_sha256": bench.kernel_source_hash()}
     path = str(tmp_path / "traffic.md")
+    summ["per_kernel"] = {"vbq_mv_pair_kernel<8,1>": {"launches": 2, "hbm_bytes_per_launch": 20}}
     bench.write_traffic_file(path, summ)
     monkeypatch.setattr(bench, "TRAFFIC_FILE", path)
     assert bench.measured_traffic(bench.TRAFFIC_CONFIG) == 15
+    assert bench.measured_traffic_per_kernel(bench.TRAFFIC_CONFIG) == {"vbq_mv_pair_kernel<8,1>": 20}
     assert bench.measured_traffic("workload 4, M 1, widths mixed") is None  # another configuration
     summ["kernel_source_sha256"] = "0" * 64                                 # another kernel source
     bench.write_traffic_file(path, summ)
@@ -80,3 +85,12 @@ def test_qat_cpu_baseline_leg():
     assert out["cores"] >= 1 and str(n) in out["sample"]
     assert bench.QAT_BYTES_PER_GROUP == 256 + 256 + 16 + 16 + 16 + 1
     assert np.isfinite(out["value"])
+
+
+def test_profiler_kernel_names_match_the_library_names():
+    """rocprofv3 prints template arguments with spaces and the default argument;
+    the per-kernel traffic is keyed by vbq_kernel_name's form."""
+    assert bench.canonical_kernel("void (anonymous namespace)::vbq_mv_kernel<1, 16, -1>(unsigned short const*, "
+                                  "unsigned char const*)") == "vbq_mv_kernel<1,16>"
+    assert bench.canonical_kernel("(anonymous namespace)::vbq_mv_kernel<1, 8, 2>(x)") == "vbq_mv_kernel<1,8,2>"
+    assert bench.canonical_kernel("vbq_mv_pair_kernel<16, 1>(a, b)") == "vbq_mv_pair_kernel<16,1>"
