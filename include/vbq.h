@@ -282,8 +282,68 @@ vbq_status vbq_gemm_small(const vbq_desc* desc, const void* blob_dev,
                           int64_t M, const void* X_dev, int64_t ldx,
                           void* Y_dev, int64_t ldy, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * One launch per decode step (paper section 6, "The speedup grows with model
+ * size": for small models the per-token overhead, not bandwidth, bounds
+ * decode).  A step is a sequence of GEMVs in which GEMV i reads its x only
+ * after every earlier GEMV of the step has written its y, as when x_i is
+ * computed from y_(i-1).  vbq_step_run runs the whole sequence in one
+ * cooperative launch: the weights of GEMV i are loaded while GEMV i-1 is
+ * still running, and only x, the multiply and the store of y wait for it.
+ * Each y is bitwise the y that vbq_gemv / vbq_gemv_rows give.
+ * ------------------------------------------------------------------------- */
+#define VBQ_STEP_MAX_GEMVS 65536
+
+/* One GEMV of a step. */
+typedef struct vbq_step_gemv {
+  const vbq_desc* desc;  /* host descriptor of the packed matrix; its
+                            VBQ_Y_F16 flag applies (VBQ_ONE_WAVE_PER_UNIT is
+                            refused)                                         */
+  const void* blob;      /* device blob, 256-byte aligned                    */
+  const void* x;         /* device fp16[K], 16-byte aligned                  */
+  void* y;               /* device float32 (fp16 with VBQ_Y_F16): y[N], or
+                            y[y_len] written through rows                    */
+  const int32_t* rows;   /* device int32[N] row map as in vbq_gemv_rows, or
+                            NULL for y[n]                                    */
+  int64_t y_len;         /* length of y when rows != NULL                    */
+} vbq_step_gemv;
+
+/* Bytes of the device plan of n GEMVs (1 <= n <= VBQ_STEP_MAX_GEMVS). */
+vbq_status vbq_step_plan_bytes(int32_t n, size_t* bytes);
+
+/* Bytes of the device workspace of vbq_step_run for n GEMVs: eight arrival
+ * words per GEMV, then one status word. */
+vbq_status vbq_step_workspace_bytes(int32_t n, size_t* bytes);
+
+/* Writes the plan of n GEMVs, run in array order, into plan_host (host
+ * memory of plan_bytes >= vbq_step_plan_bytes bytes, 8-byte aligned).  The
+ * caller copies it to device memory as it is; it stays valid while every
+ * blob, x, y and rows buffer it names does.  Every matrix must have at most 8
+ * units per row tile with at most 32 group columns each (the library's
+ * default geometry for K <= 16384).  Errors: NULL, SHAPE, DESC, BUFFER
+ * (misaligned buffers, plan too small), UNSUPPORTED (geometry outside that
+ * range, VBQ_ONE_WAVE_PER_UNIT, unknown flags, blob >= 4 GiB). */
+vbq_status vbq_step_plan(const vbq_step_gemv* gemvs, int32_t n, void* plan_host,
+                         size_t plan_bytes);
+
+/* Runs a plan of n GEMVs on stream: a small kernel that clears the workspace,
+ * then one cooperative launch of one 16-wave workgroup per CU (the grid is
+ * sized from the device's CU count and an occupancy query, and the launch
+ * fails with VBQ_ERR_HIP rather than run a grid that does not fit).
+ * plan_dev: the plan in device memory (8-byte aligned); workspace_dev: device
+ * memory of workspace_bytes >= vbq_step_workspace_bytes (4-byte aligned),
+ * caller-owned, not shared by runs that may overlap.  spin_limit bounds every
+ * wait for an earlier GEMV (polls of about 0.1 us; 0 = 2^22): a workgroup that
+ * reaches it stops waiting, skips its remaining work and sets the status word
+ * (the workspace's last uint32) to 1, so the launch always ends; the status
+ * word is 0 after a complete run.  Errors: NULL, SHAPE, BUFFER, HIP. */
+vbq_status vbq_step_run(const void* plan_dev, int32_t n, void* workspace_dev,
+                        size_t workspace_bytes, uint32_t spin_limit,
+                        void* stream);
+
 /* Name of the kernel that vbq_gemm_small with M activation rows (vbq_gemv and
- * vbq_gemv_rows for M = 1) launches on this matrix, e.g.
+ * vbq_gemv_rows for M = 1) launches on this matrix, named with its template
+ * arguments as a profiler prints them without spaces, e.g.
  * "vbq_mv_pair_kernel<8,1>" (static storage; "none" for an invalid descriptor
  * or M outside [1, 16]).  The choice depends on the widths present, the grid
  * and the flags; a caller or a profile can group launches by it. */

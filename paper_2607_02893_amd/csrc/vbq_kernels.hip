@@ -1760,17 +1760,19 @@ vbq_status launch_mm(const DevMatrix& m, uint32_t flags, const void* x, int64_t 
 // Name of the kernel a product with M activation rows launches on this matrix
 // (the same choices as launch_mv / launch_mm); static storage.
 const char* kernel_name(const DevMatrix& m, uint32_t flags, int M) {
+  // (template arguments as the compiler prints them, spaces removed; the
+  // uniform kernel's last argument is the width class log2 b)
   static const char* const kNames[] = {
       "vbq_mv_pair_kernel<8,1>", "vbq_mv_pair_kernel<16,1>", "vbq_mv_pair_kernel<8,2>",
       "vbq_mv_kernel<1,4>", "vbq_mv_kernel<1,8>", "vbq_mv_kernel<1,16>",
       "vbq_mv_kernel<2,4>", "vbq_mv_kernel<2,8>",
-      "vbq_mv_kernel<1,4,1-bit>", "vbq_mv_kernel<1,8,1-bit>", "vbq_mv_kernel<1,16,1-bit>",
-      "vbq_mv_kernel<1,4,2-bit>", "vbq_mv_kernel<1,8,2-bit>", "vbq_mv_kernel<1,16,2-bit>",
-      "vbq_mv_kernel<1,4,4-bit>", "vbq_mv_kernel<1,8,4-bit>", "vbq_mv_kernel<1,16,4-bit>",
-      "vbq_mv_kernel<1,4,8-bit>", "vbq_mv_kernel<1,8,8-bit>", "vbq_mv_kernel<1,16,8-bit>",
-      "vbq_mm_kernel<4,16-row blocks>", "vbq_mm_kernel<8,16-row blocks>", "vbq_mm_kernel<16,16-row blocks>",
-      "vbq_mm_kernel<4,32-row blocks>", "vbq_mm_kernel<8,32-row blocks>", "vbq_mm_kernel<16,32-row blocks>",
-      "vbq_mm_kernel<4,64-row blocks>", "vbq_mm_kernel<8,64-row blocks>", "vbq_mm_kernel<16,64-row blocks>",
+      "vbq_mv_kernel<1,4,0>", "vbq_mv_kernel<1,8,0>", "vbq_mv_kernel<1,16,0>",
+      "vbq_mv_kernel<1,4,1>", "vbq_mv_kernel<1,8,1>", "vbq_mv_kernel<1,16,1>",
+      "vbq_mv_kernel<1,4,2>", "vbq_mv_kernel<1,8,2>", "vbq_mv_kernel<1,16,2>",
+      "vbq_mv_kernel<1,4,3>", "vbq_mv_kernel<1,8,3>", "vbq_mv_kernel<1,16,3>",
+      "vbq_mm_kernel<4,1>", "vbq_mm_kernel<8,1>", "vbq_mm_kernel<16,1>",
+      "vbq_mm_kernel<4,2>", "vbq_mm_kernel<8,2>", "vbq_mm_kernel<16,2>",
+      "vbq_mm_kernel<4,4>", "vbq_mm_kernel<8,4>", "vbq_mm_kernel<16,4>",
       "none"};
   auto nw_index = [](int NW) { return NW == 4 ? 0 : NW == 8 ? 1 : 2; };
   if (M <= 0) return kNames[29];
@@ -1796,6 +1798,253 @@ const char* kernel_name(const DevMatrix& m, uint32_t flags, int M) {
   const int rb = m.R == 16 ? 0 : m.R == 32 ? 1 : 2;
   return kNames[20 + 3 * rb + nw_index(NW)];
 }
+
+// ---------------------------------------------------------------------------
+// One launch per decode step (paper section 6, "The speedup grows with model
+// size": at small sizes the per-token overhead, not bandwidth, bounds decode).
+//
+// A step is a sequence of GEMVs in which GEMV i may read its x only once every
+// earlier GEMV has written its y (in a model, x_i is computed from y_(i-1)).
+// One persistent grid, one workgroup of 16 waves per CU, walks the sequence:
+//   * GEMV i's row tiles are dealt to the workgroups in turn; a tile is worked
+//     by wave pairs exactly as in vbq_mv_pair_kernel (the same per-entry
+//     products, per-unit row sums and unit order, so y is bitwise the y of
+//     the one-launch-per-GEMV path), two tiles at a time when they have at
+//     most four units;
+//   * the weights do not depend on x, so before waiting for GEMV i-1 a
+//     workgroup issues the loads of its first tile of GEMV i (unit-table
+//     rows, width map, the first code batch of every class) and builds the
+//     entry index from the width map; only x, the decode, the row sums and
+//     the stores of y follow the wait;
+//   * a workgroup that has stored all its rows of GEMV i adds 1 to one of
+//     eight arrival counters of GEMV i (spread over eight words so the
+//     atomics do not all meet on one address); a workgroup waits for GEMV i
+//     by polling the eight words until they sum to the number of workgroups.
+// Cross-workgroup visibility without cache flushes: y is written with
+// device-coherent stores (agent scope), each wave waits until its stores have
+// completed before its workgroup arrives, and x is read with device-coherent
+// loads issued after the wait, so no release or acquire of the whole L2 is
+// needed.  Waits are bounded: a workgroup that polls longer than the spin
+// limit sets the status word, stops waiting and skips its remaining work
+// (still arriving everywhere), so the grid always drains.
+// ---------------------------------------------------------------------------
+constexpr int kStepWaves = 16;
+constexpr int kStepPairs = kStepWaves / 2;
+constexpr int kStepSlots = 8;  // arrival words per GEMV
+
+struct StepOp {
+  DevMatrix m;
+  const uint16_t* x;
+  void* y;
+  const int32_t* rows;  // row map (as vbq_gemv_rows) or nullptr
+  int64_t ylen;
+  int32_t yf16;
+  int32_t pad;
+};
+
+// x of one row for a window of `cols` group columns starting at column j,
+// read with device-coherent loads (lanes past the window read the last chunk).
+__device__ __forceinline__ void load_x1_coherent(const uint16_t* x, int K, int j, int cols, XRegs& xr,
+                                                 uint32_t lane) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void*)x, 0, 2 * K, 0x00020000);
+  const int n = cols * 8;
+#pragma unroll
+  for (int k = 0; k < kXRegs; ++k) {
+    const int i = max(min((int)lane + 64 * k, n - 1), 0);
+    // cache policy 16: the sc1 bit, the device-scope coherence of an agent-scope atomic load
+    xr.v[k] = __builtin_amdgcn_raw_buffer_load_b128(r, 128 * j + 16 * i, 0, 16);
+  }
+}
+
+__device__ __forceinline__ void store_y_coherent(void* y, size_t i, float v, int32_t f16) {
+  if (f16)
+    __hip_atomic_store((uint16_t*)y + i, __builtin_bit_cast(uint16_t, (_Float16)v), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  else
+    __hip_atomic_store((float*)y + i, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Waits until GEMV `op` has n_wg arrivals (wave 0 polls the eight words,
+// lanes 0..7 one each) or the spin limit is reached; every wave of the
+// workgroup calls it and gets the result through LDS.  False on a timeout.
+__device__ __forceinline__ bool step_wait(const uint32_t* sync, int op, uint32_t n_wg, uint32_t spin_limit,
+                                          uint32_t flag_lds, int wave, uint32_t lane) {
+  if (wave == 0) {
+    const uint32_t* w = sync + (size_t)op * kStepSlots + min(lane, (uint32_t)kStepSlots - 1);
+    uint32_t ok = 0;
+    for (uint32_t it = 0; it < spin_limit; ++it) {
+      const uint32_t v = lane < kStepSlots ? __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+      if (wave_sum(v) >= n_wg) {
+        ok = 1;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    if (lane == 0) lds_store_f32(flag_lds, ok ? 1.0f : 0.0f);
+  }
+  __syncthreads();
+  return lds_f32(flag_lds) != 0.0f;
+}
+
+// The arrival words of GEMV op: the unit to wait for when a later GEMV starts.
+__global__ __launch_bounds__(kStepWaves * 64) void vbq_step_kernel(const StepOp* __restrict__ plan, int n_ops,
+                                                                   uint32_t* __restrict__ sync,
+                                                                   uint32_t spin_limit) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
+  const uint32_t flag_lds = lds0;  // 16 bytes: the wait's result
+  const uint32_t base = lds0 + 16;
+  const int wave = wave_id();
+  // pair k = waves k and k + 8, which land on the same SIMD (see vbq_mv_pair_kernel)
+  const int pair = wave % kStepPairs, role = wave / kStepPairs;
+  const int wg = blockIdx.x, n_wg = gridDim.x;
+  uint32_t* status = sync + (size_t)n_ops * kStepSlots;
+  bool live = true;  // workgroup-uniform: false after a timed-out wait
+  for (int op = 0; op < n_ops; ++op) {
+    const StepOp* o = plan + op;
+    DevMatrix mat = o->m;
+    const int R = mat.R, U = mat.U, T = mat.T;
+    const int tpr = U <= kStepPairs / 2 ? 2 : 1;  // tiles per round
+    const int ups = kStepPairs / tpr;              // unit slots per tile
+    const int slot = pair / ups, k = pair % ups;
+    const WavePlan P = wave_plan(R, mat.C, 1);
+    const uint32_t ysum0 = base;  // pair p's unit row sums at ysum0 + p*R*4
+    const uint32_t ysum = ysum0 + (uint32_t)(pair * R * 4);
+    const uint32_t region = base + (uint32_t)(kStepPairs * R * 4 + pair * P.bytes);
+    Win wn;
+    wn.xs = region + P.xs;
+    wn.Xs = region + P.Xs;
+    wn.part = region + P.part;
+    wn.xstride_m = (uint32_t)(mat.C * kXStride);
+    wn.part_m = (uint32_t)(mat.C * R * 4);
+    wn.SW = mat.C;
+    wn.logR = mat.logR;
+    const uint32_t inv = region + P.inv;
+    const int my_tiles = wg < T ? (T - wg + n_wg - 1) / n_wg : 0;
+    const int rounds = (my_tiles + tpr - 1) / tpr;
+    for (int rd = 0; rd < rounds; ++rd) {
+      const uint32_t lane = lane_id_here();  // (values derived from it are not hoisted out of the loops)
+      const int ti = rd * tpr + slot;
+      const int t = wg + ti * n_wg;
+      const bool active = ti < my_tiles && k < U;  // wave-uniform
+      const bool must_wait = rd == 0 && op > 0;    // workgroup-uniform
+      const UnitInfo u = load_unit(mat, active ? t : 0, active ? k : 0);
+      const int unit = (active ? t : 0) * mat.U + (active ? k : 0);
+      uint32_t start[4], seg[4];
+      int n[4];
+      WinCounts wc;
+      // The two roles run separate code paths with the same sequence of
+      // workgroup barriers, so each keeps only its own batches in registers.
+      if (role == 0) {
+        // ---- before the wait: what depends on the weights only
+        for (int i = (int)lane; i < R; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
+        Batch<0, 1> A0;
+        if (active && live) {
+          const WmapRegs wr = load_wmap(mat, u, u.W, lane);
+          const u32x16 rows2 = unit_rows(mat, unit);
+          const u32x4 erow = rows2.s0123, own = rows2.s89ab - rows2.s0123;
+          wc.own[0] = own.x;
+          wc.own[1] = own.y;
+          wc.own[2] = own.z;
+          wc.own[3] = own.w;
+          const uint32_t es[4] = {erow.x, erow.y, erow.z, erow.w};
+          uint32_t acc = 0;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            wc.before[c] = 0u;
+            start[c] = es[c];
+            n[c] = clamp_run(mat, c, start[c], wc.own[c]);
+            seg[c] = inv + 2u * acc;
+            acc += wc.own[c];
+          }
+          load_batch<0, 1>(A0, mat, start[0], n[0], 0, lane);
+          build_index(wr, u, 0, u.W, R, wc, inv, lane);
+        }
+        if (must_wait && live && !step_wait(sync, op - 1, (uint32_t)n_wg, spin_limit, flag_lds, wave, lane)) {
+          live = false;
+          if (wave == 0 && lane == 0) __hip_atomic_store(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        __syncthreads();  // the index and x of every unit are in LDS
+        if (active && live) run_class<0, 1>(mat, A0, start[0], n[0], seg[0], wn, lane);
+        __syncthreads();  // every partial product is in LDS
+        if (active && live) reduce_window<1>(wn, R, u.cols, u.rows, ysum, lane);
+        __syncthreads();
+      } else {
+        Batch<1, 1> A1;
+        Batch<2, 1> A2;
+        Batch<3, 1> A3;
+        if (active && live) {
+          const u32x16 rows2 = unit_rows(mat, unit);
+          const u32x4 erow = rows2.s0123, own = rows2.s89ab - rows2.s0123;
+          const uint32_t es[4] = {erow.x, erow.y, erow.z, erow.w};
+          const uint32_t ow[4] = {own.x, own.y, own.z, own.w};
+          uint32_t acc = 0;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            start[c] = es[c];
+            n[c] = clamp_run(mat, c, start[c], ow[c]);
+            seg[c] = inv + 2u * acc;
+            acc += ow[c];
+          }
+          load_batch<1, 1>(A1, mat, start[1], n[1], 0, lane);
+          load_batch<2, 1>(A2, mat, start[2], n[2], 0, lane);
+          load_batch<3, 1>(A3, mat, start[3], n[3], 0, lane);
+        }
+        if (must_wait && live && !step_wait(sync, op - 1, (uint32_t)n_wg, spin_limit, flag_lds, wave, lane))
+          live = false;
+        if (active && live) {
+          XRegs xr;
+          load_x1_coherent(o->x, mat.K, u.j0, u.cols, xr, lane);
+          store_x1(u.cols, xr, wn, lane);
+        }
+        __syncthreads();  // the index and x of every unit are in LDS
+        if (active && live) {
+          run_class<1, 1>(mat, A1, start[1], n[1], seg[1], wn, lane);
+          run_class<2, 1>(mat, A2, start[2], n[2], seg[2], wn, lane);
+          run_class<3, 1>(mat, A3, start[3], n[3], seg[3], wn, lane);
+        }
+        __syncthreads();  // every partial product is in LDS
+        __syncthreads();  // (role 0 adds the row sums)
+      }
+      // per tile slot: the unit row sums added in unit order, stored coherently
+      for (int i = threadIdx.x; i < tpr * R; i += kStepWaves * 64) {
+        const int sl = i / R, r = i - sl * R;
+        const int tt = wg + (rd * tpr + sl) * n_wg;
+        if (live && rd * tpr + sl < my_tiles && r < min(R, mat.N - tt * R)) {
+          float tot = 0.0f;
+          for (int kk = 0; kk < U; ++kk) tot += lds_f32(ysum0 + 4u * (uint32_t)((sl * ups + kk) * R + r));
+          const size_t row = (size_t)tt * R + r;
+          if (o->rows == nullptr) {
+            store_y_coherent(o->y, row, tot, o->yf16);
+          } else {
+            const int64_t d = o->rows[row];
+            if (d >= 0 && d < o->ylen) store_y_coherent(o->y, (size_t)d, tot, o->yf16);
+          }
+        }
+      }
+      __syncthreads();  // LDS is reused by the next round
+    }
+    // arrival: every wave's stores of y have completed, then one atomic
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0)
+      __hip_atomic_fetch_add(sync + (size_t)op * kStepSlots + (wg & (kStepSlots - 1)), 1u, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Clears the arrival words and the status word before a step.
+__global__ __launch_bounds__(256) void vbq_step_clear_kernel(uint32_t* sync, uint32_t words) {
+  for (uint32_t i = threadIdx.x + blockIdx.x * 256u; i < words; i += 256u * gridDim.x) sync[i] = 0u;
+}
+
+// Bytes of LDS one step-kernel workgroup needs for a matrix (16-byte flag,
+// then eight pairs' row sums and regions).
+inline int step_lds_bytes(const DevMatrix& m) {
+  return 16 + kStepPairs * (m.R * 4 + wave_plan(m.R, m.C, 1).bytes);
+}
+
+uint32_t step_sync_words(int n) { return (uint32_t)n * kStepSlots + 1u; }
 
 }  // namespace
 
@@ -1885,6 +2134,82 @@ vbq_status vbq_dequant(const vbq_desc* desc, const void* blob_dev, float* W_dev,
   const int lds = kDequantWaves * region;
   return hip_status(hipLaunchKernel((const void*)vbq_dequant_kernel, dim3((unsigned)m.T), dim3(kDequantWaves * 64), args,
                                     (size_t)lds, (hipStream_t)stream));
+}
+
+vbq_status vbq_step_plan_bytes(int32_t n, size_t* bytes) {
+  if (!bytes) return VBQ_ERR_NULL;
+  if (n < 1 || n > VBQ_STEP_MAX_GEMVS) return VBQ_ERR_SHAPE;
+  *bytes = (size_t)n * sizeof(StepOp);
+  return VBQ_OK;
+}
+
+vbq_status vbq_step_workspace_bytes(int32_t n, size_t* bytes) {
+  if (!bytes) return VBQ_ERR_NULL;
+  if (n < 1 || n > VBQ_STEP_MAX_GEMVS) return VBQ_ERR_SHAPE;
+  *bytes = (size_t)step_sync_words(n) * 4;
+  return VBQ_OK;
+}
+
+vbq_status vbq_step_plan(const vbq_step_gemv* gemvs, int32_t n, void* plan_host, size_t plan_bytes) {
+  if (!gemvs || !plan_host) return VBQ_ERR_NULL;
+  if (n < 1 || n > VBQ_STEP_MAX_GEMVS) return VBQ_ERR_SHAPE;
+  if (plan_bytes < (size_t)n * sizeof(StepOp) || (uintptr_t)plan_host % 8) return VBQ_ERR_BUFFER;
+  StepOp* ops = (StepOp*)plan_host;
+  for (int32_t i = 0; i < n; ++i) {
+    const vbq_step_gemv& g = gemvs[i];
+    if (!g.desc || !g.x || !g.y) return VBQ_ERR_NULL;
+    StepOp op{};
+    vbq_status st = make_dev_matrix(g.desc, g.blob, &op.m);
+    if (st != VBQ_OK) return st;
+    if (g.desc->flags & VBQ_ONE_WAVE_PER_UNIT) return VBQ_ERR_UNSUPPORTED;
+    // the tile body is the wave-pair one: at most eight units of at most 32 columns
+    if (op.m.U > kStepPairs || op.m.C > kXRegs * 8 || step_lds_bytes(op.m) > kLdsLimit) return VBQ_ERR_UNSUPPORTED;
+    if ((uintptr_t)g.x % 16 || (uintptr_t)g.y % y_align(g.desc)) return VBQ_ERR_BUFFER;
+    if (g.rows && ((uintptr_t)g.rows % 4 || g.y_len < 0)) return g.y_len < 0 ? VBQ_ERR_SHAPE : VBQ_ERR_BUFFER;
+    op.x = (const uint16_t*)g.x;
+    op.y = g.y;
+    op.rows = g.rows;
+    op.ylen = g.rows ? g.y_len : 0;
+    op.yf16 = (g.desc->flags & VBQ_Y_F16) ? 1 : 0;
+    ops[i] = op;
+  }
+  return VBQ_OK;
+}
+
+vbq_status vbq_step_run(const void* plan_dev, int32_t n, void* workspace_dev, size_t workspace_bytes,
+                        uint32_t spin_limit, void* stream) {
+  if (!plan_dev || !workspace_dev) return VBQ_ERR_NULL;
+  if (n < 1 || n > VBQ_STEP_MAX_GEMVS) return VBQ_ERR_SHAPE;
+  const uint32_t words = step_sync_words(n);
+  if (workspace_bytes < (size_t)words * 4 || (uintptr_t)workspace_dev % 4 || (uintptr_t)plan_dev % 8)
+    return VBQ_ERR_BUFFER;
+  if (spin_limit == 0) spin_limit = 1u << 22;
+  const void* kernel = (const void*)vbq_step_kernel;
+  static std::atomic<uint64_t> done{0};
+  vbq_status st = allow_big_lds(kernel, done);
+  if (st != VBQ_OK) return st;
+  // one workgroup of 16 waves per CU, all resident at once (checked here, and
+  // the cooperative launch refuses a grid that does not fit)
+  int dev = 0, cus = 0, per_cu = 0;
+  if ((st = hip_status(hipGetDevice(&dev))) != VBQ_OK) return st;
+  if ((st = hip_status(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev))) != VBQ_OK) return st;
+  const size_t lds = kLdsLimit;
+  if ((st = hip_status(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kStepWaves * 64, lds))) !=
+      VBQ_OK)
+    return st;
+  if (per_cu < 1 || cus < 1) return VBQ_ERR_UNSUPPORTED;
+  const unsigned grid = (unsigned)cus;
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t* sync = (uint32_t*)workspace_dev;
+  {
+    void* args[] = {&sync, (void*)&words};
+    st = hip_status(hipLaunchKernel((const void*)vbq_step_clear_kernel, dim3(1), dim3(256), args, 0, s));
+    if (st != VBQ_OK) return st;
+  }
+  const StepOp* plan = (const StepOp*)plan_dev;
+  int nops = n;
+  void* args[] = {&plan, &nops, &sync, &spin_limit};
+  return hip_status(hipLaunchCooperativeKernel(kernel, dim3(grid), dim3(kStepWaves * 64), args, lds, s));
 }
 
 }  // extern "C"

@@ -56,7 +56,8 @@ STATUS = {0: "VBQ_OK", 1: "VBQ_ERR_NULL", 2: "VBQ_ERR_SHAPE", 3: "VBQ_ERR_BITS",
 # exported symbols, in the order include/vbq.h declares them
 EXPORTS = ("vbq_status_string", "vbq_last_hip_error", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
            "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_pack_row_buckets_size", "vbq_pack_row_buckets",
-           "vbq_gemv_buckets", "vbq_gemm_small", "vbq_kernel_name", "vbq_dequant",
+           "vbq_gemv_buckets", "vbq_gemm_small", "vbq_step_plan_bytes", "vbq_step_workspace_bytes",
+           "vbq_step_plan", "vbq_step_run", "vbq_kernel_name", "vbq_dequant",
            "vbq_qat_workspace_size", "vbq_qat_forward", "vbq_qat_logit_grad", "vbq_read_ceiling")
 # vbq_desc.flags (call options)
 Y_F16 = 1
@@ -88,6 +89,11 @@ class VbqDesc(ctypes.Structure):
 class VbqBucket(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_int32), ("reserved", ctypes.c_int32), ("row_begin", ctypes.c_int64),
                 ("n_rows", ctypes.c_int64), ("blob_offset", ctypes.c_uint64), ("desc", VbqDesc)]
+
+
+class VbqStepGemv(ctypes.Structure):
+    _fields_ = [("desc", ctypes.POINTER(VbqDesc)), ("blob", ctypes.c_void_p), ("x", ctypes.c_void_p),
+                ("y", ctypes.c_void_p), ("rows", ctypes.c_void_p), ("y_len", ctypes.c_int64)]
 
 
 class VbqPackOpts(ctypes.Structure):
@@ -128,6 +134,14 @@ _lib.vbq_gemv_buckets.argtypes = [ctypes.POINTER(VbqBucket), ctypes.c_int32, _P,
 _lib.vbq_gemm_small.restype = ctypes.c_int
 _lib.vbq_gemm_small.argtypes = [ctypes.POINTER(VbqDesc), _P, ctypes.c_int64, _P, ctypes.c_int64, _P,
                                 ctypes.c_int64, _P]
+_lib.vbq_step_plan_bytes.restype = ctypes.c_int
+_lib.vbq_step_plan_bytes.argtypes = [ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
+_lib.vbq_step_workspace_bytes.restype = ctypes.c_int
+_lib.vbq_step_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
+_lib.vbq_step_plan.restype = ctypes.c_int
+_lib.vbq_step_plan.argtypes = [ctypes.POINTER(VbqStepGemv), ctypes.c_int32, _P, ctypes.c_size_t]
+_lib.vbq_step_run.restype = ctypes.c_int
+_lib.vbq_step_run.argtypes = [_P, ctypes.c_int32, _P, ctypes.c_size_t, ctypes.c_uint32, _P]
 _lib.vbq_kernel_name.restype = ctypes.c_char_p
 _lib.vbq_kernel_name.argtypes = [ctypes.POINTER(VbqDesc), ctypes.c_int64]
 _lib.vbq_read_ceiling.restype = ctypes.c_int
@@ -262,6 +276,40 @@ def pack_row_buckets(q, scales, bits, tile_rows=0, chunk_groups=0, n_threads=0):
 
 def desc_check(d):
     return _lib.vbq_desc_check(ctypes.byref(d))
+
+
+class Step:
+    """A decode step run as one launch (vbq_step_run): a sequence of GEMVs, GEMV
+    i reading its x only after every earlier GEMV has written its y.
+
+    gemvs: list of (desc, blob_ptr, x_ptr, y_ptr, rows_ptr or 0, y_len) on one
+    device; the plan and the workspace are allocated here with torch (device
+    memory), and the host plan image is built by vbq_step_plan."""
+
+    def __init__(self, gemvs, device="cuda"):
+        import torch
+        n = len(gemvs)
+        self.n = n
+        self._descs = [VbqDesc.from_buffer_copy(g[0]) for g in gemvs]  # kept alive for the plan call
+        arr = (VbqStepGemv * n)()
+        for i, (g, d) in enumerate(zip(gemvs, self._descs)):
+            arr[i] = VbqStepGemv(ctypes.pointer(d), g[1], g[2], g[3], g[4] or None, int(g[5]))
+        pb, wb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+        _check(_lib.vbq_step_plan_bytes(n, ctypes.byref(pb)), "vbq_step_plan_bytes")
+        _check(_lib.vbq_step_workspace_bytes(n, ctypes.byref(wb)), "vbq_step_workspace_bytes")
+        host = np.zeros(pb.value, dtype=np.uint8)
+        _check(_lib.vbq_step_plan(arr, n, _ptr(host), pb.value), "vbq_step_plan")
+        self.plan = torch.from_numpy(host).to(device)
+        self.workspace = torch.zeros(wb.value // 4, dtype=torch.int32, device=device)
+
+    def run(self, stream=None, spin_limit=0):
+        return _lib.vbq_step_run(ctypes.c_void_p(self.plan.data_ptr()), self.n,
+                                 ctypes.c_void_p(self.workspace.data_ptr()), self.workspace.numel() * 4,
+                                 int(spin_limit), _stream_handle(stream))
+
+    def status(self):
+        """The status word (0 after a complete run); synchronizes."""
+        return int(self.workspace[-1].item())
 
 
 def kernel_name(d, M=1):

@@ -284,6 +284,45 @@ def test_pack_row_buckets_c_abi():
     assert lib.vbq_gemv_buckets(out, 1, None, None, None, None, 0, None) == 1
 
 
+def test_step_plan_argument_errors():
+    """vbq_step_plan / _bytes / _run check everything on the host first."""
+    lib = vbq.lib()
+    nb = ctypes.c_size_t(0)
+    assert lib.vbq_step_plan_bytes(0, ctypes.byref(nb)) == 2
+    assert lib.vbq_step_plan_bytes(1, None) == 1
+    assert lib.vbq_step_plan_bytes(3, ctypes.byref(nb)) == 0 and nb.value > 0
+    per = nb.value // 3
+    assert lib.vbq_step_workspace_bytes(3, ctypes.byref(nb)) == 0 and nb.value == 4 * (8 * 3 + 1)
+    rng = synth.rng_for(6)
+    bits, q, s = _random_codes(rng, 40, 1024)
+    _, d = vbq.pack_codes(q, s, bits)
+    A = 1 << 20
+    plan = np.zeros(4 * per, dtype=np.uint8)
+
+    def plan_of(desc, x=A, y=A, rows=None, y_len=0, n=1, buf=plan):
+        g = (vbq.VbqStepGemv * 1)(vbq.VbqStepGemv(ctypes.pointer(desc), A, x, y, rows, y_len))
+        return lib.vbq_step_plan(g, n, buf.ctypes.data_as(ctypes.c_void_p), buf.nbytes)
+    assert plan_of(d) == 0
+    assert plan_of(d, n=0) == 2
+    assert plan_of(d, x=A + 8) == 7                 # x misaligned
+    assert plan_of(d, y=A + 2) == 7                 # float y misaligned
+    assert plan_of(d, x=0) == 1
+    small = np.zeros(per - 8, dtype=np.uint8)
+    assert plan_of(d, buf=small) == 7               # plan buffer too small
+    assert plan_of(d, rows=A + 2, y_len=40) == 7    # row map misaligned
+    assert plan_of(d, rows=A, y_len=-1) == 2
+    d.flags = vbq.ONE_WAVE_PER_UNIT
+    assert plan_of(d) == 10
+    d.flags = 0
+    _, dwide = vbq.pack_codes(q, s, bits, chunk_groups=1)  # 16 units per tile: beyond the pair body
+    assert plan_of(dwide) == 10
+    bad = vbq.VbqDesc()
+    assert plan_of(bad) == 8
+    assert lib.vbq_step_run(None, 1, ctypes.c_void_p(A), 64, 0, None) == 1
+    assert lib.vbq_step_run(ctypes.c_void_p(A), 2, ctypes.c_void_p(A), 4 * 8, 0, None) == 7  # workspace too small
+    assert lib.vbq_step_run(ctypes.c_void_p(A), 0, ctypes.c_void_p(A), 64, 0, None) == 2
+
+
 def test_single_hip_runtime():
     """libvbq must share torch's HIP runtime: one libamdhip64 in the process."""
     assert len(vbq.hip_runtimes()) == 1
