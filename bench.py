@@ -541,6 +541,8 @@ def main():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs of --profile (FETCH_SIZE, WRITE_SIZE) and exit")
     ap.add_argument("--write-traffic", metavar="PATH", help="with --pmc-summary: write the traffic summary file")
+    ap.add_argument("--persistent", action="store_true",
+                    help="time the step as one launch (vbq_step_run) instead of one launch per GEMV")
     ap.add_argument("--qat", action="store_true",
                     help="time the selection-path forward (training) over the 131M-class weights instead")
     args = ap.parse_args()
@@ -580,6 +582,8 @@ def main():
     for _ in range(args.warmup):
         st.run(stream.cuda_stream)
     torch.cuda.synchronize()
+    if args.persistent:
+        return main_persistent(args, wl, st, stream)
     g = st.graph(stream)
 
     if args.profile:
@@ -718,6 +722,75 @@ def main():
         "per_shape": per_shape,
         "cpu_baseline": cpu,
         "dense_fp16_baseline": dense,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def main_persistent(args, wl, st, stream):
+    """--persistent: the same step as ONE launch (vbq_step_run): the GEMVs in
+    order, each waiting for the previous one inside the kernel."""
+    import torch
+    from paper_2607_02893_amd import vbq
+    ps = vbq.Step(st.launch_args)
+    ref = [m[2].clone() for m in st.mats]  # per-GEMV launches (warm-up above)
+    for m in st.mats:
+        m[2].fill_(float("nan"))
+
+    def run():
+        r = ps.run(stream)
+        if r != 0:
+            raise vbq.VbqError(r, "vbq_step_run")
+    run()
+    torch.cuda.synchronize()
+    if ps.status() != 0:
+        raise RuntimeError("vbq_step_run: a wait timed out")
+    same = all(torch.equal(r, m[2]) for r, m in zip(ref, st.mats))
+    log(f"one-launch step equals the per-GEMV launches bit for bit: {same}")
+    if not same:
+        raise RuntimeError("one-launch step differs from the per-GEMV launches")
+    for _ in range(args.warmup):
+        run()
+    if args.profile:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            run()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        print(json.dumps({"profile_run": True, "persistent": True, "us_per_step": round(1e6 * dt, 2)}), flush=True)
+        return
+    wall_s, gpu_s = timed(run, args.steps, stream)
+    dist = distribution(run, min(100, args.steps), stream)
+    torch.cuda.synchronize()
+    assert ps.status() == 0
+    # the per-GEMV path on the same tree, for comparison
+    g = st.graph(stream)
+    for _ in range(args.warmup):
+        g.replay()
+    per_s, _ = timed(g.replay, args.steps, stream)
+    log(f"one launch: {1e6 * wall_s:.1f} us/step (events {1e6 * gpu_s:.1f}); one launch per GEMV "
+        f"(graph): {1e6 * per_s:.1f} us/step")
+    value = st.total_alg / wall_s / 1e9
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(1e3 * wall_s, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32",
+        "precision": "fp16 activations x {1,2,4,8}-bit codes with fp16 group scales, fp32 accumulation",
+        "data": "synthetic (seeded draws; no trained weights)",
+        "config": {"workload": f"{wl.name} decode step (workload {args.workload}) as one launch: "
+                               f"{len(st.launch_args)} GEMVs, {st.total_w / 1e9:.2f}G weights", "M": 1,
+                   "algorithmic_bytes_per_step": int(st.total_alg),
+                   "timing": "eager vbq_step_run calls (a clearing kernel + one cooperative launch)"},
+        "us_per_step": round(1e6 * wall_s, 2), "us_per_step_distribution": dist,
+        "us_per_step_per_gemv_launches": round(1e6 * per_s, 2),
+        "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBS, 1),
+        "roofline": {"bound": "hbm", "achieved": round(st.total_alg / gpu_s / 1e9, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(st.total_alg / gpu_s / 1e9 / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": "vbq_step_kernel", "launches_per_step": 1,
+                     "algorithmic_bytes_per_launch": int(st.total_alg), "avg_launch_us": round(1e6 * gpu_s, 2),
+                     "timing": "HIP events on the launch stream around K steps"},
+        "bitwise_equal_to_per_gemv_launches": same,
+        "cpu_baseline": None,
     }
     print(json.dumps(out), flush=True)
 

@@ -312,7 +312,8 @@ typedef struct vbq_step_gemv {
 vbq_status vbq_step_plan_bytes(int32_t n, size_t* bytes);
 
 /* Bytes of the device workspace of vbq_step_run for n GEMVs: eight arrival
- * words per GEMV, then one status word. */
+ * words per GEMV, each in its own 128-byte line (1 KiB per GEMV), then one
+ * status word. */
 vbq_status vbq_step_workspace_bytes(int32_t n, size_t* bytes);
 
 /* Writes the plan of n GEMVs, run in array order, into plan_host (host

@@ -292,7 +292,7 @@ def test_step_plan_argument_errors():
     assert lib.vbq_step_plan_bytes(1, None) == 1
     assert lib.vbq_step_plan_bytes(3, ctypes.byref(nb)) == 0 and nb.value > 0
     per = nb.value // 3
-    assert lib.vbq_step_workspace_bytes(3, ctypes.byref(nb)) == 0 and nb.value == 4 * (8 * 3 + 1)
+    assert lib.vbq_step_workspace_bytes(3, ctypes.byref(nb)) == 0 and nb.value == 4 * (8 * 32 * 3 + 1)
     rng = synth.rng_for(6)
     bits, q, s = _random_codes(rng, 40, 1024)
     _, d = vbq.pack_codes(q, s, bits)
@@ -319,7 +319,7 @@ def test_step_plan_argument_errors():
     bad = vbq.VbqDesc()
     assert plan_of(bad) == 8
     assert lib.vbq_step_run(None, 1, ctypes.c_void_p(A), 64, 0, None) == 1
-    assert lib.vbq_step_run(ctypes.c_void_p(A), 2, ctypes.c_void_p(A), 4 * 8, 0, None) == 7  # workspace too small
+    assert lib.vbq_step_run(ctypes.c_void_p(A), 2, ctypes.c_void_p(A), 4 * 8 * 32, 0, None) == 7  # workspace too small
     assert lib.vbq_step_run(ctypes.c_void_p(A), 0, ctypes.c_void_p(A), 64, 0, None) == 2
 
 
