@@ -342,6 +342,22 @@ vbq_status vbq_step_run(const void* plan_dev, int32_t n, void* workspace_dev,
                         size_t workspace_bytes, uint32_t spin_limit,
                         void* stream);
 
+/* vbq_step_run without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that
+ * forbid hipMalloc): the arrival words live in a scratch array the library
+ * holds in device memory, 512 KiB per GPU it runs on, from the first call
+ * on that GPU until the process ends.  No call allocates anything.
+ *   n            1 .. 512 GEMVs (VBQ_ERR_SHAPE beyond; vbq_step_run has no
+ *                such limit).
+ *   status_dev   device uint32 (4-byte aligned) that receives the status word
+ *                of vbq_step_run (0 complete, 1 a wait gave up), or NULL.
+ * Every call on one GPU shares that GPU's scratch, which the call clears
+ * first: calls that may overlap on one GPU (other streams, other threads)
+ * race and must be serialized by the caller.  Errors: NULL, SHAPE, BUFFER,
+ * UNSUPPORTED (device index >= 64), HIP. */
+vbq_status vbq_step_run_noalloc(const void* plan_dev, int32_t n, uint32_t spin_limit,
+                                uint32_t* status_dev, void* stream);
+
 /* Name of the kernel that vbq_gemm_small with M activation rows (vbq_gemv and
  * vbq_gemv_rows for M = 1) launches on this matrix, named with its template
  * arguments as a profiler prints them without spaces, e.g.

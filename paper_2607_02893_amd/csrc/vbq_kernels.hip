@@ -28,6 +28,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <mutex>
 #include <cstdint>
 #include <type_traits>
 
@@ -1895,6 +1896,7 @@ __device__ __forceinline__ bool step_wait(const uint32_t* sync, int op, uint32_t
 // The arrival words of GEMV op: the unit to wait for when a later GEMV starts.
 __global__ __launch_bounds__(kStepWaves * 64) void vbq_step_kernel(const StepOp* __restrict__ plan, int n_ops,
                                                                    uint32_t* __restrict__ sync,
+                                                                   uint32_t* __restrict__ status,
                                                                    uint32_t spin_limit) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
@@ -1904,7 +1906,6 @@ __global__ __launch_bounds__(kStepWaves * 64) void vbq_step_kernel(const StepOp*
   // pair k = waves k and k + 8, which land on the same SIMD (see vbq_mv_pair_kernel)
   const int pair = wave % kStepPairs, role = wave / kStepPairs;
   const int wg = blockIdx.x, n_wg = gridDim.x;
-  uint32_t* status = sync + (size_t)n_ops * kStepSlots * kStepSlotStride;
   bool live = true;  // workgroup-uniform: false after a timed-out wait
   for (int op = 0; op < n_ops; ++op) {
     const StepOp* o = plan + op;
@@ -2040,8 +2041,9 @@ __global__ __launch_bounds__(kStepWaves * 64) void vbq_step_kernel(const StepOp*
 }
 
 // Clears the arrival words and the status word before a step.
-__global__ __launch_bounds__(256) void vbq_step_clear_kernel(uint32_t* sync, uint32_t words) {
+__global__ __launch_bounds__(256) void vbq_step_clear_kernel(uint32_t* sync, uint32_t words, uint32_t* status) {
   for (uint32_t i = threadIdx.x + blockIdx.x * 256u; i < words; i += 256u * gridDim.x) sync[i] = 0u;
+  if (threadIdx.x == 0 && blockIdx.x == 0) *status = 0u;
 }
 
 // Bytes of LDS one step-kernel workgroup needs for a matrix (16-byte flag,
@@ -2050,7 +2052,42 @@ inline int step_lds_bytes(const DevMatrix& m) {
   return 16 + kStepPairs * (m.R * 4 + wave_plan(m.R, m.C, 1).bytes);
 }
 
-uint32_t step_sync_words(int n) { return (uint32_t)n * kStepSlots * kStepSlotStride + 1u; }
+uint32_t step_arrival_words(int n) { return (uint32_t)n * kStepSlots * kStepSlotStride; }
+uint32_t step_sync_words(int n) { return step_arrival_words(n) + 1u; }  // + the status word
+
+vbq_status launch_step(const void* plan_dev, int32_t n, uint32_t* sync, uint32_t* status, uint32_t spin_limit,
+                       void* stream);
+
+// Scratch of vbq_step_run_noalloc: the arrival words and the status word of a
+// step of up to kNoAllocMaxGemvs GEMVs (512 KiB; every GPU the library runs on
+// holds its own copy until the process ends).  Host code never uses this name
+// as an address: it is a host-side stand-in, and the device address comes from
+// hipGetSymbolAddress, once per device.
+constexpr int kNoAllocMaxGemvs = 512;
+constexpr int kNoAllocWords = kNoAllocMaxGemvs * kStepSlots * kStepSlotStride + 64;
+static __device__ __align__(256) uint32_t scratch[kNoAllocWords];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint32_t* g_scratch_dev[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up on the first call per device.
+vbq_status scratch_address(uint32_t** out) {
+  int dev = 0;
+  vbq_status st = hip_status(hipGetDevice(&dev));
+  if (st != VBQ_OK) return st;
+  if (dev < 0 || dev >= kMaxDevices) return VBQ_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    st = hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (st != VBQ_OK) return st;
+    if (!p) return VBQ_ERR_HIP;
+    g_scratch_dev[dev] = (uint32_t*)p;
+  }
+  *out = g_scratch_dev[dev];
+  return VBQ_OK;
+}
 
 }  // namespace
 
@@ -2189,7 +2226,32 @@ vbq_status vbq_step_run(const void* plan_dev, int32_t n, void* workspace_dev, si
   const uint32_t words = step_sync_words(n);
   if (workspace_bytes < (size_t)words * 4 || (uintptr_t)workspace_dev % 4 || (uintptr_t)plan_dev % 8)
     return VBQ_ERR_BUFFER;
+  uint32_t* sync = (uint32_t*)workspace_dev;
+  return launch_step(plan_dev, n, sync, sync + step_arrival_words(n), spin_limit, stream);
+}
+
+vbq_status vbq_step_run_noalloc(const void* plan_dev, int32_t n, uint32_t spin_limit, uint32_t* status_dev,
+                                void* stream) {
+  if (!plan_dev) return VBQ_ERR_NULL;
+  if (n < 1 || n > kNoAllocMaxGemvs) return VBQ_ERR_SHAPE;
+  if ((uintptr_t)plan_dev % 8 || (uintptr_t)status_dev % 4) return VBQ_ERR_BUFFER;
+  uint32_t* sync = nullptr;
+  vbq_status st = scratch_address(&sync);
+  if (st != VBQ_OK) return st;
+  // the status word: the caller's, or the last word of the scratch
+  return launch_step(plan_dev, n, sync, status_dev ? status_dev : sync + (kNoAllocWords - 1), spin_limit, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// The clearing kernel and the cooperative launch of the step kernel over the
+// arrival words `sync` (step_arrival_words(n) words) and the status word.
+vbq_status launch_step(const void* plan_dev, int32_t n, uint32_t* sync, uint32_t* status, uint32_t spin_limit,
+                       void* stream) {
   if (spin_limit == 0) spin_limit = 1u << 22;
+  const uint32_t words = step_arrival_words(n);
   const void* kernel = (const void*)vbq_step_kernel;
   static std::atomic<uint64_t> done{0};
   vbq_status st = allow_big_lds(kernel, done);
@@ -2206,16 +2268,15 @@ vbq_status vbq_step_run(const void* plan_dev, int32_t n, void* workspace_dev, si
   if (per_cu < 1 || cus < 1) return VBQ_ERR_UNSUPPORTED;
   const unsigned grid = (unsigned)cus;
   hipStream_t s = (hipStream_t)stream;
-  uint32_t* sync = (uint32_t*)workspace_dev;
   {
-    void* args[] = {&sync, (void*)&words};
+    void* args[] = {&sync, (void*)&words, &status};
     st = hip_status(hipLaunchKernel((const void*)vbq_step_clear_kernel, dim3(1), dim3(256), args, 0, s));
     if (st != VBQ_OK) return st;
   }
   const StepOp* plan = (const StepOp*)plan_dev;
   int nops = n;
-  void* args[] = {&plan, &nops, &sync, &spin_limit};
+  void* args[] = {&plan, &nops, &sync, &status, &spin_limit};
   return hip_status(hipLaunchCooperativeKernel(kernel, dim3(grid), dim3(kStepWaves * 64), args, lds, s));
 }
 
-}  // extern "C"
+}  // namespace

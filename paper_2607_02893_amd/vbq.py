@@ -57,7 +57,7 @@ STATUS = {0: "VBQ_OK", 1: "VBQ_ERR_NULL", 2: "VBQ_ERR_SHAPE", 3: "VBQ_ERR_BITS",
 EXPORTS = ("vbq_status_string", "vbq_last_hip_error", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
            "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_pack_row_buckets_size", "vbq_pack_row_buckets",
            "vbq_gemv_buckets", "vbq_gemm_small", "vbq_step_plan_bytes", "vbq_step_workspace_bytes",
-           "vbq_step_plan", "vbq_step_run", "vbq_kernel_name", "vbq_dequant",
+           "vbq_step_plan", "vbq_step_run", "vbq_step_run_noalloc", "vbq_kernel_name", "vbq_dequant",
            "vbq_qat_workspace_size", "vbq_qat_forward", "vbq_qat_logit_grad", "vbq_read_ceiling")
 # vbq_desc.flags (call options)
 Y_F16 = 1
@@ -142,6 +142,8 @@ _lib.vbq_step_plan.restype = ctypes.c_int
 _lib.vbq_step_plan.argtypes = [ctypes.POINTER(VbqStepGemv), ctypes.c_int32, _P, ctypes.c_size_t]
 _lib.vbq_step_run.restype = ctypes.c_int
 _lib.vbq_step_run.argtypes = [_P, ctypes.c_int32, _P, ctypes.c_size_t, ctypes.c_uint32, _P]
+_lib.vbq_step_run_noalloc.restype = ctypes.c_int
+_lib.vbq_step_run_noalloc.argtypes = [_P, ctypes.c_int32, ctypes.c_uint32, _P, _P]
 _lib.vbq_kernel_name.restype = ctypes.c_char_p
 _lib.vbq_kernel_name.argtypes = [ctypes.POINTER(VbqDesc), ctypes.c_int64]
 _lib.vbq_read_ceiling.restype = ctypes.c_int
@@ -306,6 +308,13 @@ class Step:
         return _lib.vbq_step_run(ctypes.c_void_p(self.plan.data_ptr()), self.n,
                                  ctypes.c_void_p(self.workspace.data_ptr()), self.workspace.numel() * 4,
                                  int(spin_limit), _stream_handle(stream))
+
+    def run_noalloc(self, status=None, stream=None, spin_limit=0):
+        """vbq_step_run_noalloc (the library's own scratch); status: an optional
+        int32 device tensor of one element that receives the status word."""
+        return _lib.vbq_step_run_noalloc(ctypes.c_void_p(self.plan.data_ptr()), self.n, int(spin_limit),
+                                         ctypes.c_void_p(status.data_ptr()) if status is not None else None,
+                                         _stream_handle(stream))
 
     def status(self):
         """The status word (0 after a complete run); synchronizes."""
