@@ -284,23 +284,26 @@ __host__ __device__ inline int align16(int v) { return (v + 15) & ~15; }
 // Byte offsets inside one wave's LDS region (window of SW columns, R rows,
 // MT activation rows).
 struct WavePlan {
-  int inv, xs, Xs, part, bytes;
+  int inv, xs, Xs, part, tab, bytes;
 };
 
-__host__ __device__ inline WavePlan wave_plan(int R, int SW, int MT) {
+// tab_bytes: the 1-bit lookup tables of one group column (kLutBytes) for the
+// one-width 1-bit kernel, else 0.
+__host__ __device__ inline WavePlan wave_plan(int R, int SW, int MT, int tab_bytes = 0) {
   WavePlan p;
   int o = 0;
   p.inv = o;  o += align16(SW * R * 2);  // uint16 local position of each entry
   p.xs = o;   o += MT * SW * kXStride;   // staged x
   p.Xs = o;   o += align16(MT * SW * 4); // per-column activation sums
   p.part = o; o += MT * SW * R * 4;      // per-entry partial products
+  p.tab = o;  o += tab_bytes;            // 1-bit lookup tables
   p.bytes = o;
   return p;
 }
 
 // Whole workgroup: NW row-sum arrays (MT*R floats each), then NW regions.
-__host__ __device__ inline int mv_lds_bytes(int R, int SW, int MT, int NW) {
-  return NW * (MT * R * 4 + wave_plan(R, SW, MT).bytes);
+__host__ __device__ inline int mv_lds_bytes(int R, int SW, int MT, int NW, int tab_bytes = 0) {
+  return NW * (MT * R * 4 + wave_plan(R, SW, MT, tab_bytes).bytes);
 }
 
 // Group columns per width-map word (1 when a column spans whole words).
@@ -557,7 +560,7 @@ __device__ __forceinline__ void load_batch(Batch<CLS, MT>& bt, const DevMatrix& 
 }
 
 struct Win {  // LDS byte addresses of the wave's window buffers
-  uint32_t xs, Xs, part;
+  uint32_t xs, Xs, part, tab;
   uint32_t xstride_m;  // bytes between the staged x rows
   uint32_t part_m;     // bytes between the partial-product planes of two x rows
   int SW, logR;        // window columns (Xs row stride), log2 R
@@ -654,28 +657,120 @@ __device__ __forceinline__ void decode_batch(const Batch<CLS, MT>& bt, uint32_t 
   }
 }
 
+// ---------------------------------------------------------------------------
+// 1-bit decode through lookup tables (one-width 1-bit matrices, full tiles of
+// at least 64 rows, where a 64-entry slot is 64 rows of ONE group column).
+//
+// A 1-bit group's 64 codes are 16 nibbles: nibble n of word w holds the codes
+// of weights i0 + 2t, t = 0..3, with i0 = 32w + 8(n & 3) + (n >> 2) (the even
+// weights of the word's pairs in its low half-word, the odd ones in the high
+// half-word).  For the slot's group column, table m = 8w + n holds the 16
+// subset sums T_m[v] = sum over the set bits t of v of x[i0 + 2t] (fp32), so
+// the sum of x over the group's 1-codes is sum_m T_m[nibble m]: 16 lookups
+// instead of 32 masks and 32 two-term dot products.  The 16 entries of a
+// table sit in 16 consecutive words, so the 64 lanes' lookups into one table
+// never meet in a bank.  Then sum q x = 2 sum_{u=1} x - X_j as in the dot2
+// path.  A table costs each lane one 16-byte read of x, a few adds and one
+// 16-byte store, once per group column (every R/64 slots).
+// ---------------------------------------------------------------------------
+constexpr int kLutBytes = 16 * 16 * 4;  // 16 tables of 16 fp32 entries
+
+// Lane l writes entries 4(l & 3) .. +3 of table l >> 2 for group column js.
+__device__ __forceinline__ void build_lut(int js, const Win& wn, uint32_t lane) {
+  const uint32_t m = lane >> 2, hi = lane & 3u;
+  const uint32_t w = m >> 3, n = m & 7u, e = n >> 2;
+  const uint32_t q = 4u * w + (n & 3u);  // x chunk of weights i0 .. i0 + 7
+  const u32x4 c = lds_u32x4(wn.xs + (uint32_t)__umul24((uint32_t)js, kXStride) + 16u * q);
+  const uint32_t sh = 16u * e;  // weight i0 + 2t is half e of dword t
+  const float x0 = (float)__builtin_bit_cast(_Float16, (uint16_t)(c.x >> sh));
+  const float x1 = (float)__builtin_bit_cast(_Float16, (uint16_t)(c.y >> sh));
+  const float x2 = (float)__builtin_bit_cast(_Float16, (uint16_t)(c.z >> sh));
+  const float x3 = (float)__builtin_bit_cast(_Float16, (uint16_t)(c.w >> sh));
+  const float th = ((hi & 1u) ? x2 : 0.0f) + ((hi & 2u) ? x3 : 0.0f);  // bits 2, 3 of v = 4 hi + lo
+  u32x4 t;
+  t.x = __float_as_uint(th);
+  t.y = __float_as_uint(th + x0);
+  t.z = __float_as_uint(th + x1);
+  t.w = __float_as_uint(th + (x0 + x1));
+  lds_store_u32x4(wn.tab + 64u * m + 16u * hi, t);
+}
+
+// decode_batch for one-width 1-bit windows of full tiles with R >= 64: slot i
+// of batch b is entries g0 .. g0 + 63, all in group column g0 / R, and the
+// slot that starts a column first builds its tables.
+__device__ __forceinline__ void decode_batch_lut(const Batch<0, 1>& bt, int n, int b, uint32_t lane,
+                                                 const Win& wn) {
+  constexpr int E = Batch<0, 1>::E;
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    const int g0 = (b * E + i) * 64;
+    if (g0 < n) {  // wave-uniform: whole slots past the end are skipped
+      const int js = g0 >> wn.logR;
+      if ((g0 & ((1 << wn.logR) - 1)) == 0) {
+        lds_phase();
+        build_lut(js, wn, lane);
+        lds_phase();
+      }
+      const float X = lds_f32(wn.Xs + 4u * (uint32_t)js);
+      const uint32_t w0 = bt.w[2 * i], w1 = bt.w[2 * i + 1];
+      // table m's entry for nibble m: one bit-field extract and one shift-add
+      // per lookup (written out: the compiler's shift, mask and add take three)
+      uint32_t tab_v;
+      __asm__("v_mov_b32 %0, %1" : "=v"(tab_v) : "s"(wn.tab));
+      float acc = 0.0f;
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        const uint32_t word = m < 8 ? w0 : w1;
+        uint32_t a;
+        __asm__("v_bfe_u32 %0, %1, %2, 4\n\tv_lshl_add_u32 %0, %0, 2, %3"
+                : "=&v"(a)
+                : "v"(word), "n"(4 * (m & 7)), "v"(tab_v));
+        const float t = lds_f32(a + 64u * (uint32_t)m);
+        acc = m == 0 ? t : acc + t;
+      }
+      const float s = (float)__builtin_bit_cast(_Float16, bt.s[i]);
+      // lanes past the end hold the run's last entry: same value, same place
+      const int p = min(g0 + (int)lane, n - 1);
+      lds_store_f32(wn.part + 4u * (uint32_t)p, s * __builtin_fmaf(acc, 2.0f, -X));
+      lds_phase();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // The n entries of class CLS of the window, starting at entry `start` of the
 // class section.  Batch 0 is already in A (loaded with the other classes'
 // first batches); the next batch is in flight while the current one is
 // decoded.  The loop runs at least once and its loads are unconditional
 // (past the last batch they repeat it), so the count of outstanding loads
 // never depends on the data.
-template <int CLS, int MT, bool kUni = false>
+// kLut: the 1-bit lookup-table decode (one-width 1-bit windows of full tiles
+// with R >= 64 only).
+template <int CLS, int MT, bool kUni, bool kLut>
+__device__ __forceinline__ void decode_any(const Batch<CLS, MT>& bt, uint32_t inv_c, int n, int b, uint32_t lane,
+                                           const Win& wn) {
+  if constexpr (kLut)
+    decode_batch_lut(bt, n, b, lane, wn);
+  else
+    decode_batch<CLS, MT, kUni>(bt, inv_c, n, b, lane, wn);
+}
+
+template <int CLS, int MT, bool kUni = false, bool kLut = false>
 __device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS, MT>& A, uint32_t start, int n,
                                           uint32_t inv_c, const Win& wn, uint32_t lane) {
   constexpr int per_batch = Batch<CLS, MT>::E * Batch<CLS, MT>::G;
   const int nb = max(1, (n + per_batch - 1) / per_batch);
   if (MT == 1 && nb == 1) {  // wave-uniform: no further batch, so no prefetch (each path keeps exact wait counts)
-    decode_batch<CLS, MT, kUni>(A, inv_c, n, 0, lane, wn);
+    decode_any<CLS, MT, kUni, kLut>(A, inv_c, n, 0, lane, wn);
     return;
   }
   Batch<CLS, MT> B;
   for (int b = 0; b < nb; b += 2) {
     load_batch<CLS, MT>(B, mat, start, n, min(b + 1, nb - 1), lane);
-    decode_batch<CLS, MT, kUni>(A, inv_c, n, b, lane, wn);
+    decode_any<CLS, MT, kUni, kLut>(A, inv_c, n, b, lane, wn);
     if (b + 1 >= nb) break;
     load_batch<CLS, MT>(A, mat, start, n, min(b + 2, nb - 1), lane);
-    decode_batch<CLS, MT, kUni>(B, inv_c, n, b + 1, lane, wn);
+    decode_any<CLS, MT, kUni, kLut>(B, inv_c, n, b + 1, lane, wn);
   }
 }
 
@@ -843,13 +938,14 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
   const int wave = wave_id();
   const int t = blockIdx.x;  // one row tile per workgroup
   const int NS = MT * R;
-  const WavePlan P = wave_plan(R, SW, MT);
+  const WavePlan P = wave_plan(R, SW, MT, UNI == 0 ? kLutBytes : 0);
   const uint32_t ysum = lds0 + (uint32_t)(wave * NS * 4);
   const uint32_t region = lds0 + (uint32_t)(NW * NS * 4 + wave * P.bytes);
   Win wn;
   wn.xs = region + P.xs;
   wn.Xs = region + P.Xs;
   wn.part = region + P.part;
+  wn.tab = region + P.tab;
   wn.xstride_m = (uint32_t)(SW * kXStride);
   wn.part_m = (uint32_t)(SW * R * 4);
   wn.SW = SW;
@@ -878,7 +974,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       load_batch<UNI, MT>(A, mat, first, n, 0, lane);
       store_x1(cols, xr, wn, lane);
       lds_phase();
-      run_class<UNI, MT, true>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
+      if (UNI == 0 && MT == 1 && R >= 64 && u.rows == R)  // wave-uniform: slots of one column each
+        run_class<UNI, MT, true, UNI == 0 && MT == 1>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
+      else
+        run_class<UNI, MT, true>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
       lds_phase();
       reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
       lds_phase();
@@ -1671,6 +1770,9 @@ vbq_status launch_mv(const DevMatrix& m, uint32_t flags, const void* x, int64_t 
         ++classes;
       }
     if (classes == 1) {
+      // the 1-bit kernel holds one group column's lookup tables per wave
+      if (uni == 0) sh.lds = mv_lds_bytes(m.R, sh.SW, 1, sh.NW, kLutBytes);
+      if (sh.lds > kLdsLimit) return VBQ_ERR_UNSUPPORTED;
       switch (uni * 3 + (sh.NW == 4 ? 0 : sh.NW == 8 ? 1 : 2)) {
         case 0: return launch_mv_nw<1, 4, 0>(a, sh.lds, s);
         case 1: return launch_mv_nw<1, 8, 0>(a, sh.lds, s);

@@ -49,7 +49,7 @@ def _oracle_rows(q, s, x, block=8192):
 
 
 def _probe_columns(K):
-    return sorted({0, 1, 63, 64, K // 2 + 17, K - 65, K - 1})
+    return sorted(k for k in {0, 1, 63, 64, K // 2 + 17, K - 65, K - 1} if 0 <= k < K)
 
 
 def _probe_groups(Gc):
@@ -140,6 +140,7 @@ UNIFORM = [
     ("recipe down L0 (4-bit)", "recipe", "down", 0),
     ("uniform 8-bit o (1.46B-class)", "u8", "o", 0),
     ("uniform 1-bit qkv (1.46B-class)", "u1", "qkv", 0),
+    ("uniform 1-bit head (1.46B-class, 64-row tiles: lookup-table decode)", "u1", "head", 32),
 ]
 
 
@@ -154,6 +155,20 @@ def test_exact_probes_uniform_kernels(vbq, what, kind, name, layer):
     Wp = vbq.PackedMatrix(blob, d)
     call, call16 = _gemv_calls(Wp)
     _suite(call, q, s, bits, spec.K, what, 103, call16)
+
+
+@pytest.mark.parametrize("N,K,R", [(1000, 4096, 64), (700, 2048, 128), (1300, 1024, 256), (64, 64, 64)])
+def test_exact_probes_lut_decode_tile_heights(vbq, N, K, R):
+    """The 1-bit lookup-table decode (full tiles of one-width 1-bit matrices
+    with R >= 64: a table per group column, rebuilt every R/64 slots), with a
+    ragged last tile on the two-term dot-product path, every row exact."""
+    spec = synth.MatrixSpec("u", 0, 1, N, K, uniform_bits=1)
+    bits, q, s = synth.make_matrix(spec, 151)
+    blob, d = vbq.pack_codes(q, s, bits, tile_rows=R)
+    Wp = vbq.PackedMatrix(blob, d)
+    assert vbq.kernel_name(d).startswith("vbq_mv_kernel<1,") and vbq.kernel_name(d).endswith(",0>")
+    call, call16 = _gemv_calls(Wp)
+    _suite(call, q, s, bits, K, f"1-bit lookup tables N={N} K={K} R={R}", 157, call16)
 
 
 def test_exact_probes_bucketed_head(vbq):
