@@ -1266,43 +1266,69 @@ struct MmArgs {
   int32_t yf16;       // 1: y holds fp16
 };
 
-// Bytes of one wave's LDS region: row sums (16 x R floats) and the
-// position -> entry map (uint16 per position of the widest slice).
+// Bytes of one wave's LDS region: row sums (16 x R floats), the per-class
+// table of the slice (five rows of eight words), and the position -> entry
+// map (uint16 per position of the widest slice).
+constexpr int kMmTableBytes = 5 * 32;
 __host__ __device__ inline int mm_wave_bytes(int R, int cols) {
-  return kMmRows * R * 4 + align16(((cols * R + 63) / 64) * 64 * 2);
+  return kMmRows * R * 4 + kMmTableBytes + align16(((cols * R + 63) / 64) * 64 * 2);
 }
 
-// Per-class values of the slice.
-struct MmClassInfo {
-  uint32_t start[4];  // first entry of the slice's run in each class section
-  uint32_t lim[4];    // last entry of each class section (0 when empty)
-  uint32_t offc[4], offs[4];
-};
-
-// v[c] for a per-lane c, without memory access.
-__device__ __forceinline__ uint32_t sel4(const uint32_t v[4], uint32_t c) {
-  const uint32_t lo = (c & 1u) ? v[1] : v[0], hi = (c & 1u) ? v[3] : v[2];
-  return (c & 2u) ? hi : lo;
+// The table a lane reads for its block's entry, row c of width class c (row
+// 4: class 0 for lanes with odd h, whose 1-bit fields sit 8 bits higher):
+//   word 0..3  code section offset, scale section offset, slice run start,
+//              last entry of the class section (addresses of the entry);
+//   word 4     field mask of one pair (two codes, one per half-word): 1 bit
+//              codes are read from the word rotated right by 31 (even h:
+//              fields 0..7 move up one bit) or by 7 (odd h: fields 8..15 move
+//              down seven), so a field shifted by its offset lands at bit 1 of
+//              each half, and no field crosses the word's ends;
+//   word 5     -(1024 + offset) in both fp16 halves: a masked field ORed into
+//              1024.0 reads as 1024 + u (1024 + 2u for 1 bit), and one
+//              packed add makes the level q exactly (1025 for 1 bit, 1024 +
+//              2^(b-1) otherwise: integers below 2048, exact in fp16);
+//   word 6     the field's bit offset (in the rotated word) for products
+//              kb = 0..3, one per byte;
+//   word 7     the pair's second field offset b | (3 + c) << 8 (log2 of the
+//              entry's bytes) | c << 16 | rotation << 24.
+// Row `row` of the table (lane 0 of the wave writes all five once per slice;
+// the values are wave-uniform): code and scale section offsets, the slice's
+// run start and the class section's last entry.
+template <int row>
+__device__ __forceinline__ void write_mm_row(uint32_t tab, uint32_t offc, uint32_t offs, uint32_t start,
+                                             uint32_t lim) {
+  constexpr uint32_t c = row == 4 ? 0u : (uint32_t)row;
+  constexpr uint32_t kMask[4] = {0x00020002u, 0x00030003u, 0x000F000Fu, 0x00FF00FFu};
+  constexpr uint32_t kSub[4] = {0xE401E401u, 0xE402E402u, 0xE408E408u, 0xE480E480u};
+  constexpr uint32_t kShift[4] = {0x06040200u, 0x0C080400u, 0x08000800u, 0u};
+  constexpr uint32_t rot = row == 4 ? 7u : row == 0 ? 31u : 0u;
+  lds_store_u32x4(tab + 32u * row, u32x4{offc, offs, start, lim});
+  lds_store_u32x4(tab + 32u * row + 16u,
+                  u32x4{kMask[c], kSub[c], kShift[c], (1u << c) | ((3u + c) << 8) | (c << 16) | (rot << 24)});
 }
 
 // One block in registers for this lane: its entry's 16 code bytes that hold
-// the lane's 16 levels, the width class, the scale (0 for a padding row), and
-// 16 activations of row l % 16.
+// the lane's 16 levels, the class table's decoding words, the fp16 scale bits
+// (zero-extended), and 16 activations of row l % 16.  A lane of a padding row
+// (past the matrix's last row) decodes a clamped in-range entry: its product
+// column is that row's alone and is never added to a row sum, so no value
+// loaded for it needs a select (which would wait for the load).
 struct MmBlock {
   u32x4 w;
-  uint32_t c;
-  uint16_t s;
+  u32x4 k;   // table words 4..7 of the entry's class
+  uint32_t s;
   u32x4 a0, a1;
 };
 
 // Block f of the row group: column f / RB, row block rg*RB + f % RB.  The
 // lane's levels 16h .. 16h + 15 (h = lane / 16) are pairs 8h .. 8h + 7, whose
 // codes start at byte (2h << c) & ~3 of the entry.  Loads are unconditional
-// (clamped), so several blocks stay in flight.
+// (clamped), so several blocks stay in flight.  X comes through a buffer
+// resource (xr) covering the M rows.
 template <int RB>
-__device__ __forceinline__ void load_mm_block(MmBlock& bk, const uint16_t* xp, int64_t ldx, int M,
-                                              const DevMatrix& mat, uint32_t fwd, int f, int rg, int rows,
-                                              const MmClassInfo& ci, int j0, uint32_t lane) {
+__device__ __forceinline__ void load_mm_block(MmBlock& bk, __amdgpu_buffer_rsrc_t xr, int64_t ldx, int M,
+                                              const DevMatrix& mat, uint32_t fwd, uint32_t tab, int f, int rg,
+                                              int rows, int j0, uint32_t lane) {
   const int R = mat.R;
   const uint32_t e = lane & 15u, h = lane >> 4;
   const int col = f / RB;
@@ -1310,45 +1336,49 @@ __device__ __forceinline__ void load_mm_block(MmBlock& bk, const uint16_t* xp, i
   const uint32_t v = (uint32_t)lds_u16(fwd + 2u * (uint32_t)(col * R + row));
   const bool real = row < rows;
   const uint32_t c = real ? v >> 14 : 0u;
-  const uint32_t g = min(sel4(ci.start, c) + (real ? (v & 0x3FFFu) : 0u), sel4(ci.lim, c));
-  bk.c = c;
-  bk.w = ld<u32x4>(mat.blob, sel4(ci.offc, c) + (g << (3 + c)) + (((2u * h) << c) & ~3u));
-  const uint16_t sb = ld<uint16_t>(mat.blob, sel4(ci.offs, c) + 2u * g);
-  bk.s = real ? sb : (uint16_t)0;
+  const uint32_t trow = (c == 0u && (h & 1u)) ? 4u : c;
+  const u32x4 t0 = lds_u32x4(tab + 32u * trow);
+  bk.k = lds_u32x4(tab + 32u * trow + 16u);
+  const uint32_t g = min(t0.z + (real ? (v & 0x3FFFu) : 0u), t0.w);
+  bk.w = ld<u32x4>(mat.blob, t0.x + (g << (3 + c)) + (((2u * h) << c) & ~3u));
+  bk.s = (uint32_t)ld<uint16_t>(mat.blob, t0.y + 2u * g);
   const int m = min((int)e, M - 1);
-  const u32x4* xr = (const u32x4*)(xp + (size_t)m * ldx + (size_t)(j0 + col) * 64 + 16 * h);
-  bk.a0 = xr[0];
-  bk.a1 = xr[1];
+  const uint32_t xo = 2u * (uint32_t)((int64_t)m * ldx + (int64_t)(j0 + col) * 64 + 16 * (int)h);
+  bk.a0 = __builtin_amdgcn_raw_buffer_load_b128(xr, (int)xo, 0, 0);
+  bk.a1 = __builtin_amdgcn_raw_buffer_load_b128(xr, (int)xo + 16, 0, 0);
 }
 
-// s * D of one block.  For product kb the lane's two pairs 8h + 2kb, + 1 are
-// fields f, f + 1 of word wi of its 16 code bytes:
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+
+// s * D of one block, two 16 x 16 x 32 products (weights 16h .. 16h + 7 and
+// 16h + 8 .. 16h + 15 of the lane's entry against the same activations).
+// For kb = 0..3 the lane's pairs 8h + 2kb, + 1 are fields f, f + 1 of word
+// wi of its 16 code bytes:
 //   1 bit: wi = 0, f = 8 (h & 1) + 2kb;  2 bits: wi = 0, f = 2kb;
 //   4 bits: wi = kb / 2, f = 2 (kb & 1); 8 bits: wi = kb, f = 0.
-__device__ __forceinline__ float4_t mm_products(const MmBlock& bk, uint32_t h) {
-  const uint32_t c = bk.c, B = 1u << c;
-  const uint32_t mask = (0x00010001u << B) - 0x00010001u;
-  // q = (1024 + u - 1024) * mul + add: mul 2, add -1 for 1 bit; mul 1, add -2^(B-1)
-  const half2_t base = {(_Float16)-1024.0f, (_Float16)-1024.0f};
-  const _Float16 mul1 = c == 0 ? (_Float16)2.0f : (_Float16)1.0f;
-  const _Float16 add1 = c == 0 ? (_Float16)-1.0f : (_Float16)(-(float)(1u << (B - 1)));
-  const half2_t mul = {mul1, mul1}, add = {add1, add1};
-  const uint32_t w[4] = {bk.w.x, bk.w.y, bk.w.z, bk.w.w};
-  const uint32_t a[8] = {bk.a0.x, bk.a0.y, bk.a0.z, bk.a0.w, bk.a1.x, bk.a1.y, bk.a1.z, bk.a1.w};
-  float4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
+__device__ __forceinline__ float4_t mm_products(const MmBlock& bk) {
+  const uint32_t c = (bk.k.w >> 16) & 0xFFu, B = bk.k.w & 0xFFu;
+  const uint32_t mask = bk.k.x, sub = bk.k.y, shifts = bk.k.z;
+  const uint32_t src0 = __builtin_amdgcn_alignbit(bk.w.x, bk.w.x, bk.k.w >> 24);
+  const uint32_t src1 = c == 3u ? bk.w.y : src0;
+  const uint32_t src2 = c == 3u ? bk.w.z : c == 2u ? bk.w.y : src0;
+  const uint32_t src3 = c == 3u ? bk.w.w : c == 2u ? bk.w.y : src0;
+  const uint32_t word[4] = {src0, src1, src2, src3};
+  uint32_t q[8];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
-    const uint32_t word = c == 3 ? w[kb] : c == 2 ? w[kb >> 1] : w[0];
-    const uint32_t f = c == 0 ? 8u * (h & 1u) + 2u * kb : c == 1 ? 2u * kb : c == 2 ? 2u * (kb & 1) : 0u;
-    const uint32_t sh = f << c;
-    const uint32_t v0 = ((word >> sh) & mask) | 0x64006400u;  // 1024 + u, both halves
-    const uint32_t v1 = ((word >> (sh + B)) & mask) | 0x64006400u;
-    const half2_t q0 = (as_h2(v0) + base) * mul + add, q1 = (as_h2(v1) + base) * mul + add;
-    const half4_t bq = {q0.x, q0.y, q1.x, q1.y};
-    const half4_t ax = __builtin_bit_cast(half4_t, u32x2{a[2 * kb], a[2 * kb + 1]});
-    d = __builtin_amdgcn_mfma_f32_16x16x16f16(ax, bq, d, 0, 0, 0);
+    const uint32_t sh = (shifts >> (8 * kb)) & 0xFFu;
+    const uint32_t v0 = ((word[kb] >> sh) & mask) | 0x64006400u;  // 1024 + u (1024 + 2u for 1 bit)
+    const uint32_t v1 = ((word[kb] >> (sh + B)) & mask) | 0x64006400u;
+    q[2 * kb] = __builtin_bit_cast(uint32_t, as_h2(v0) + as_h2(sub));
+    q[2 * kb + 1] = __builtin_bit_cast(uint32_t, as_h2(v1) + as_h2(sub));
   }
-  const float s = (float)__builtin_bit_cast(_Float16, bk.s);
+  const half8_t b0 = __builtin_bit_cast(half8_t, u32x4{q[0], q[1], q[2], q[3]});
+  const half8_t b1 = __builtin_bit_cast(half8_t, u32x4{q[4], q[5], q[6], q[7]});
+  float4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
+  d = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, bk.a0), b0, d, 0, 0, 0);
+  d = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, bk.a1), b1, d, 0, 0, 0);
+  const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)bk.s);
   return d * s;
 }
 
@@ -1356,7 +1386,7 @@ __device__ __forceinline__ float4_t mm_products(const MmBlock& bk, uint32_t h) {
 // every path, so no register with a load in flight is ever reused for
 // something else (which would make the compiler wait for all loads).
 __device__ __forceinline__ void mm_done(const MmBlock& bk) {
-  __asm__ __volatile__("" ::"v"(bk.w), "v"(bk.s), "v"(bk.a0), "v"(bk.a1), "v"(bk.c));
+  __asm__ __volatile__("" ::"v"(bk.w), "v"(bk.s), "v"(bk.a0), "v"(bk.a1), "v"(bk.k));
 }
 
 // As for the one-row kernel, the values the first loads depend on come as
@@ -1364,7 +1394,7 @@ __device__ __forceinline__ void mm_done(const MmBlock& bk) {
 // the unit table is read beside the width map rather than after it, and the
 // argument block is read only once those loads are issued.
 template <int NW, int RB>
-__global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(const uint8_t* __restrict__ blob, uint32_t off_wmap,
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) void vbq_mm_kernel(const uint8_t* __restrict__ blob, uint32_t off_wmap,
                                                          uint32_t tile_words, uint32_t chunk_words, uint32_t wmap_words,
                                                          int32_t G, int32_t N, uint32_t geo, int32_t U, MmArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -1387,7 +1417,8 @@ __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(const uint8_t* __restri
   const int cmax = max_slice_cols(R, mat.C, S);
   const int wbytes = mm_wave_bytes(R, cmax);
   const uint32_t ysum = lds0 + (uint32_t)(wave * wbytes);
-  const uint32_t fwd = ysum + (uint32_t)(kMmRows * R * 4);
+  const uint32_t tab = ysum + (uint32_t)(kMmRows * R * 4);
+  const uint32_t fwd = tab + (uint32_t)kMmTableBytes;
   const int rows = min(R, mat.N - t * R);
   {
     const uint32_t lane = lane_id_here();
@@ -1412,15 +1443,21 @@ __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(const uint8_t* __restri
     const uint16_t* xp = (const uint16_t*)opaque64((uint64_t)a.x);
     const int64_t ldx = (int64_t)opaque64((uint64_t)a.ldx);
     const int M = (int)opaque((uint32_t)a.M);
+    // X rows 0 .. M-1 (fp16, stride ldx): the bytes up to the end of row M-1
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)xp, 0, (int)(2 * ((int64_t)(M - 1) * ldx + mat.K)), 0x00020000);
     const WinCounts wc = window_counts(wr, u, wb, we, R, lane);
-    MmClassInfo ci;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      ci.start[c] = uniform((int)(es[c] + wc.before[c]));
-      ci.lim[c] = uniform((int)(max(opaque(mat.n_entries[c]), 1u) - 1u));
-      ci.offc[c] = opaque(mat.off_codes[c]);
-      ci.offs[c] = opaque(mat.off_scales[c]);
+#define VBQ_MM_ROW(row, c)                                                                          \
+  write_mm_row<row>(tab, opaque(mat.off_codes[c]), opaque(mat.off_scales[c]),                       \
+                    uniform((int)(es[c] + wc.before[c])), uniform((int)(max(opaque(mat.n_entries[c]), 1u) - 1u)))
+    if (lane == 0) {
+      VBQ_MM_ROW(0, 0);
+      VBQ_MM_ROW(1, 1);
+      VBQ_MM_ROW(2, 2);
+      VBQ_MM_ROW(3, 3);
+      VBQ_MM_ROW(4, 0);
     }
+#undef VBQ_MM_ROW
     build_index<true>(wr, u, wb, we, R, wc, fwd, lane);
     lds_phase();
     const int j0 = u.j0 + cb;
@@ -1431,22 +1468,22 @@ __global__ __launch_bounds__(NW * 64) void vbq_mm_kernel(const uint8_t* __restri
 #pragma unroll
       for (int i = 0; i < RB; ++i) acc[i] = float4_t{0.0f, 0.0f, 0.0f, 0.0f};
       MmBlock B0, B1, B2, B3;
-      load_mm_block<RB>(B0, xp, ldx, M, mat, fwd, 0, rg, rows, ci, j0, lane);
-      load_mm_block<RB>(B1, xp, ldx, M, mat, fwd, min(1, last), rg, rows, ci, j0, lane);
-      load_mm_block<RB>(B2, xp, ldx, M, mat, fwd, min(2, last), rg, rows, ci, j0, lane);
+      load_mm_block<RB>(B0, xr, ldx, M, mat, fwd, tab, 0, rg, rows, j0, lane);
+      load_mm_block<RB>(B1, xr, ldx, M, mat, fwd, tab, min(1, last), rg, rows, j0, lane);
+      load_mm_block<RB>(B2, xr, ldx, M, mat, fwd, tab, min(2, last), rg, rows, j0, lane);
       // four blocks in flight; block f adds into acc[f % RB] (the ring slot)
       for (int f = 0; f < nf; f += 4) {
-        load_mm_block<RB>(B3, xp, ldx, M, mat, fwd, min(f + 3, last), rg, rows, ci, j0, lane);
-        acc[0 % RB] += mm_products(B0, h);
+        load_mm_block<RB>(B3, xr, ldx, M, mat, fwd, tab, min(f + 3, last), rg, rows, j0, lane);
+        acc[0 % RB] += mm_products(B0);
         mm_done(B0);
-        load_mm_block<RB>(B0, xp, ldx, M, mat, fwd, min(f + 4, last), rg, rows, ci, j0, lane);
-        if (f + 1 < nf) acc[1 % RB] += mm_products(B1, h);
+        load_mm_block<RB>(B0, xr, ldx, M, mat, fwd, tab, min(f + 4, last), rg, rows, j0, lane);
+        if (f + 1 < nf) acc[1 % RB] += mm_products(B1);
         mm_done(B1);
-        load_mm_block<RB>(B1, xp, ldx, M, mat, fwd, min(f + 5, last), rg, rows, ci, j0, lane);
-        if (f + 2 < nf) acc[2 % RB] += mm_products(B2, h);
+        load_mm_block<RB>(B1, xr, ldx, M, mat, fwd, tab, min(f + 5, last), rg, rows, j0, lane);
+        if (f + 2 < nf) acc[2 % RB] += mm_products(B2);
         mm_done(B2);
-        load_mm_block<RB>(B2, xp, ldx, M, mat, fwd, min(f + 6, last), rg, rows, ci, j0, lane);
-        if (f + 3 < nf) acc[3 % RB] += mm_products(B3, h);
+        load_mm_block<RB>(B2, xr, ldx, M, mat, fwd, tab, min(f + 6, last), rg, rows, j0, lane);
+        if (f + 3 < nf) acc[3 % RB] += mm_products(B3);
         mm_done(B3);
       }
       mm_done(B0);
