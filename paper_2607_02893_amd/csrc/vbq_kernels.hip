@@ -1030,8 +1030,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       }
       // the first batch of every class is in flight while x is stored and the
       // index is built (and, for several rows, x is staged): one memory
-      // latency for all four (several rows need the registers, and load the
-      // 8-bit one when its turn comes)
+      // latency for all four
       Batch<0, MT> A0;
       Batch<1, MT> A1;
       Batch<2, MT> A2;
@@ -1039,7 +1038,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       load_batch<0, MT>(A0, mat, start[0], n[0], 0, lane);
       load_batch<1, MT>(A1, mat, start[1], n[1], 0, lane);
       load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
-      if constexpr (MT == 1) load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
+      load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
       // one row: x arrived with the map and goes to LDS now
       if constexpr (MT == 1) store_x1(cols, xr, wn, lane);
       build_index(wr, u, wb, we, R, wc, inv, lane);
@@ -1048,7 +1047,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
       run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
       run_class<2, MT>(mat, A2, start[2], n[2], seg[2], wn, lane);
-      if constexpr (MT > 1) load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
       run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
       lds_phase();
       reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
@@ -1097,9 +1095,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
 // roles.  With fewer units, (2k, 2k + 1) spreads the busy waves over more SIMDs.
 //
 // MT = 2 activation rows uses the same split (x of both rows staged straight
-// from memory by role 1, the 8-bit batch loaded when its turn comes), in
-// 8-wave workgroups only: two rows need more than the 128 registers a wave of
-// a 16-wave workgroup can have.
+// from memory by role 1, every class's first batch loaded before the first
+// barrier as for one row), in 8-wave workgroups only: two rows need more than
+// the 128 registers a wave of a 16-wave workgroup can have.
 // ---------------------------------------------------------------------------
 template <int NW, int MT>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 4 : 2))) void vbq_mv_pair_kernel(
@@ -1192,12 +1190,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
     } else {
       load_batch<1, MT>(A1, mat, start[1], n[1], 0, lane);
       load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
-      if constexpr (MT == 1) {
-        load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
+      load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
+      if constexpr (MT == 1)
         store_x1(u.cols, xr, wn, lane);
-      } else {
+      else
         stage_x<MT>(a, u.j0, u.cols, wn, lane);  // (several rows: straight from memory to LDS)
-      }
     }
   }
   __syncthreads();  // the index and x of every unit are in LDS
@@ -1207,8 +1204,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
     } else {
       run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
       run_class<2, MT>(mat, A2, start[2], n[2], seg[2], wn, lane);
-      // several rows need the registers: the 8-bit batch is loaded when its turn comes
-      if constexpr (MT > 1) load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
       run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
     }
   }
