@@ -249,15 +249,17 @@ def write_traffic_file(path, summ):
     lines = [
         "# HBM traffic of vbq_mv_kernel<1>: 9B-class decode step (129 GEMVs, M=1)",
         "",
-        "Two counter passes over `bench.py --profile --steps 2 --warmup 1` (the step's HIP graph replayed 3 times),",
-        "then a plain copy of 256 MiB (torch.mul by 1.0) to scale the counters to bytes:",
+        "Two counter passes over `bench.py --profile --workers 1 --steps 2 --warmup 1` (the step's HIP graph",
+        "replayed 3 times; the weights packed in the process itself, since a worker process of the packing",
+        "pool that receives the pool's SIGTERM stalls in the counter tool's shutdown), then a plain copy of",
+        "256 MiB (torch.mul by 1.0) to scale the counters to bytes:",
         "",
         "```",
         "cd /tmp && export TMPDIR=/tmp",
         "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pmc_fetch -o run -- "
-        "python3 $R/bench.py --profile --steps 2 --warmup 1",
+        "python3 $R/bench.py --profile --workers 1 --steps 2 --warmup 1",
         "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pmc_write -o run -- "
-        "python3 $R/bench.py --profile --steps 2 --warmup 1",
+        "python3 $R/bench.py --profile --workers 1 --steps 2 --warmup 1",
         "python3 bench.py --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write --write-traffic <this file>",
         "```",
         "",
