@@ -256,14 +256,14 @@ def write_traffic_file(path, summ):
         "",
         "```",
         "cd /tmp && export TMPDIR=/tmp",
-        "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pmc_fetch -o run -- "
+        "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d $OUT/pmc_fetch -o run -- "
         "python3 $R/bench.py --profile --workers 1 --steps 2 --warmup 1",
-        "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pmc_write -o run -- "
+        "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d $OUT/pmc_write -o run -- "
         "python3 $R/bench.py --profile --workers 1 --steps 2 --warmup 1",
-        "python3 bench.py --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write --write-traffic <this file>",
+        "python3 bench.py --pmc-summary $OUT/pmc_fetch $OUT/pmc_write --write-traffic <this file>",
         "```",
         "",
-        "(`$R` is the repository root.)  Per-launch figures, averaged over every GEMV launch of the step:",
+        "(`$R` is the repository root, `$OUT` an output directory.)  Per-launch figures, averaged over every GEMV launch of the step:",
         "",
         f"- config: {TRAFFIC_CONFIG}",
         f"- launches: {summ['launches']}",
@@ -297,15 +297,15 @@ def write_qat_traffic_file(path, summ):
         "",
         "```",
         "cd /tmp && export TMPDIR=/tmp",
-        "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pmc_qat_fetch -o run -- "
+        "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d $OUT/pmc_qat_fetch -o run -- "
         "python3 $R/bench.py --qat --profile --steps 2 --warmup 1",
-        "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pmc_qat_write -o run -- "
+        "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d $OUT/pmc_qat_write -o run -- "
         "python3 $R/bench.py --qat --profile --steps 2 --warmup 1",
-        "python3 bench.py --qat --pmc-summary gpurun_out/pmc_qat_fetch gpurun_out/pmc_qat_write "
+        "python3 bench.py --qat --pmc-summary $OUT/pmc_qat_fetch $OUT/pmc_qat_write "
         "--write-traffic <this file>",
         "```",
         "",
-        "(`$R` is the repository root.)  Per-launch figures, averaged over the forward launches:",
+        "(`$R` is the repository root, `$OUT` an output directory.)  Per-launch figures, averaged over the forward launches:",
         "",
         f"- config: {QAT_TRAFFIC_CONFIG}",
         f"- launches: {summ['launches']}",
@@ -558,7 +558,7 @@ def main():
             (write_qat_traffic_file if args.qat else write_traffic_file)(args.write_traffic, summ)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the fused GEMV path has no multi-GPU mode in this build "
+        print("bench.py measures one GPU only: the fused GEMV path has no multi-GPU mode "
               "(the row / K split that would shard it is described in the design notes).", file=sys.stderr)
         sys.exit(2)
     if args.qat:
