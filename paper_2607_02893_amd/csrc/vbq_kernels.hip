@@ -815,32 +815,26 @@ __device__ __forceinline__ void store_x1(int cols, const XRegs& xr, const Win& w
   }
 }
 
-// General staging (several activation rows): x rows m < M of columns
-// [j, j + cols) and their column sums (sequential order); rows M..MT-1 are 0.
+// Several activation rows, as load_x1 / store_x1 row by row: every chunk's
+// load is issued first (rows at or past M read row M-1 and are stored as
+// zeros), so the staging costs one memory latency, not one per chunk.
 template <int MT>
-__device__ __forceinline__ void stage_x(const MvArgs& a, int j, int cols, const Win& wn, uint32_t lane) {
-  const int n = MT * cols * 8;
-  for (int i = (int)lane; i < n; i += 64) {
-    const int m = i / (cols * 8), rem = i - m * (cols * 8);
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (m < a.M) v = *(const u32x4*)(a.x + m * a.ldx + (size_t)(j + (rem >> 3)) * 64 + (rem & 7) * 8);
-    lds_store_u32x4(wn.xs + (uint32_t)m * wn.xstride_m + (uint32_t)((rem >> 3) * kXStride + (rem & 7) * 16), v);
-  }
-  lds_phase();
-  const uint32_t ones = 0x3C003C00u;
-  for (int i = (int)lane; i < MT * cols; i += 64) {
-    const int m = i / cols, jc = i - m * cols;
-    const uint32_t base = wn.xs + (uint32_t)m * wn.xstride_m + (uint32_t)(jc * kXStride);
-    float acc = 0.0f;
+__device__ __forceinline__ void load_xm(const MvArgs& a, int j, int cols, XRegs (&xr)[MT], uint32_t lane) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const u32x4 v = lds_u32x4(base + 16u * q);
-      acc = dot2(v.x, ones, acc);
-      acc = dot2(v.y, ones, acc);
-      acc = dot2(v.z, ones, acc);
-      acc = dot2(v.w, ones, acc);
+  for (int m = 0; m < MT; ++m) load_x1(a.x + (size_t)min(m, a.M - 1) * (size_t)a.ldx, j, cols, xr[m], lane);
+}
+template <int MT>
+__device__ __forceinline__ void store_xm(const MvArgs& a, int cols, XRegs (&xr)[MT], const Win& wn, uint32_t lane) {
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    if (m >= a.M) {  // wave-uniform
+#pragma unroll
+      for (int k = 0; k < kXRegs; ++k) xr[m].v[k] = u32x4{0u, 0u, 0u, 0u};
     }
-    lds_store_f32(wn.Xs + 4u * (uint32_t)(m * wn.SW + jc), acc);
+    Win w = wn;
+    w.xs = wn.xs + (uint32_t)m * wn.xstride_m;
+    w.Xs = wn.Xs + 4u * (uint32_t)(m * wn.SW);
+    store_x1(cols, xr[m], w, lane);
   }
 }
 
@@ -1018,6 +1012,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       } else {
         wc = window_counts(wr, u, wb, we, R, lane);
       }
+      XRegs xrm[MT > 1 ? MT : 1];
+      if constexpr (MT > 1) load_xm<MT>(a, u.j0 + c0, cols, xrm, lane);  // (several rows: per window)
       uint32_t start[4], seg[4];
       int n[4];
       uint32_t o = 0;
@@ -1042,7 +1038,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       // one row: x arrived with the map and goes to LDS now
       if constexpr (MT == 1) store_x1(cols, xr, wn, lane);
       build_index(wr, u, wb, we, R, wc, inv, lane);
-      if constexpr (MT > 1) stage_x<MT>(a, u.j0 + c0, cols, wn, lane);
+      if constexpr (MT > 1) store_xm<MT>(a, cols, xrm, wn, lane);
       lds_phase();
       run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
       run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
@@ -1094,10 +1090,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
 // k and k + NW/2 instead: both land on one SIMD, so every SIMD carries both
 // roles.  With fewer units, (2k, 2k + 1) spreads the busy waves over more SIMDs.
 //
-// MT = 2 activation rows uses the same split (x of both rows staged straight
-// from memory by role 1, every class's first batch loaded before the first
-// barrier as for one row), in 8-wave workgroups only: two rows need more than
-// the 128 registers a wave of a 16-wave workgroup can have.
+// MT = 2 activation rows uses the same split (x of both rows loaded by role 1
+// with the map and every class's first batch loaded before the first barrier,
+// as for one row), in 8-wave workgroups only: two rows need more than the 128
+// registers a wave of a 16-wave workgroup can have.
 // ---------------------------------------------------------------------------
 template <int NW, int MT>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 4 : 2))) void vbq_mv_pair_kernel(
@@ -1154,10 +1150,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
   if (active) {
     WmapRegs wr;
     XRegs xr;
+    XRegs xrm[MT > 1 ? MT : 1];
     if (role == 0)
       wr = load_wmap(mat, u, u.W, lane);
     else if constexpr (MT == 1)
       load_x1(x, u.j0, u.cols, xr, lane);
+    else
+      load_xm<MT>(a, u.j0, u.cols, xrm, lane);  // (several rows: with the map, like one row)
     const u32x16 rows2 = unit_rows(mat, unit);
     const u32x4 erow = rows2.s0123, own = rows2.s89ab - rows2.s0123;
     // (the class sections' offsets come from the kernel-argument block: read
@@ -1194,7 +1193,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       if constexpr (MT == 1)
         store_x1(u.cols, xr, wn, lane);
       else
-        stage_x<MT>(a, u.j0, u.cols, wn, lane);  // (several rows: straight from memory to LDS)
+        store_xm<MT>(a, u.cols, xrm, wn, lane);
     }
   }
   __syncthreads();  // the index and x of every unit are in LDS
