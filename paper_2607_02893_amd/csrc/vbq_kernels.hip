@@ -2091,11 +2091,13 @@ __global__ __launch_bounds__(kStepWaves * 64) void vbq_step_kernel(const StepOp*
           uint32_t acc = 0;
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
+            // (wave-uniform values, kept in scalar registers: the decode's vector
+            // registers are the step kernel's tightest resource)
             wc.before[c] = 0u;
-            start[c] = es[c];
-            n[c] = clamp_run(mat, c, start[c], wc.own[c]);
-            seg[c] = inv + 2u * acc;
-            acc += wc.own[c];
+            start[c] = (uint32_t)uniform((int)es[c]);
+            n[c] = uniform(clamp_run(mat, c, start[c], (uint32_t)uniform((int)wc.own[c])));
+            seg[c] = (uint32_t)uniform((int)(inv + 2u * acc));
+            acc += (uint32_t)uniform((int)wc.own[c]);
           }
           load_batch<0, 1>(A0, mat, start[0], n[0], 0, lane);
           build_index(wr, u, 0, u.W, R, wc, inv, lane);
@@ -2121,14 +2123,13 @@ __global__ __launch_bounds__(kStepWaves * 64) void vbq_step_kernel(const StepOp*
           uint32_t acc = 0;
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
-            start[c] = es[c];
-            n[c] = clamp_run(mat, c, start[c], ow[c]);
-            seg[c] = inv + 2u * acc;
-            acc += ow[c];
+            start[c] = (uint32_t)uniform((int)es[c]);
+            n[c] = uniform(clamp_run(mat, c, start[c], (uint32_t)uniform((int)ow[c])));
+            seg[c] = (uint32_t)uniform((int)(inv + 2u * acc));
+            acc += (uint32_t)uniform((int)ow[c]);
           }
           load_batch<1, 1>(A1, mat, start[1], n[1], 0, lane);
           load_batch<2, 1>(A2, mat, start[2], n[2], 0, lane);
-          load_batch<3, 1>(A3, mat, start[3], n[3], 0, lane);
         }
         if (must_wait && live && !step_wait(sync, op - 1, (uint32_t)n_wg, spin_limit, flag_lds, wave, lane))
           live = false;
@@ -2141,6 +2142,9 @@ __global__ __launch_bounds__(kStepWaves * 64) void vbq_step_kernel(const StepOp*
         if (active && live) {
           run_class<1, 1>(mat, A1, start[1], n[1], seg[1], wn, lane);
           run_class<2, 1>(mat, A2, start[2], n[2], seg[2], wn, lane);
+          // the 8-bit batch only now: held across the other classes' decode it
+          // made the kernel spill (one 1 KB scratch round trip per decoded slot)
+          load_batch<3, 1>(A3, mat, start[3], n[3], 0, lane);
           run_class<3, 1>(mat, A3, start[3], n[3], seg[3], wn, lane);
         }
         __syncthreads();  // every partial product is in LDS
