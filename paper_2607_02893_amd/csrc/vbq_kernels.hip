@@ -288,22 +288,24 @@ struct WavePlan {
 };
 
 // tab_bytes: the 1-bit lookup tables of one group column (kLutBytes) for the
-// one-width 1-bit kernel, else 0.
-__host__ __device__ inline WavePlan wave_plan(int R, int SW, int MT, int tab_bytes = 0) {
+// one-width 1-bit kernel, else 0.  index: whether the wave builds a position
+// index (one-width kernels find positions from the geometry and have none).
+__host__ __device__ inline WavePlan wave_plan(int R, int SW, int MT, int tab_bytes = 0, bool index = true) {
   WavePlan p;
   int o = 0;
-  p.inv = o;  o += align16(SW * R * 2);  // uint16 local position of each entry
+  p.tab = o;  o += tab_bytes;                      // 1-bit lookup tables (first: 256-byte aligned)
+  p.inv = o;  o += index ? align16(SW * R * 2) : 0;  // uint16 local position of each entry
   p.xs = o;   o += MT * SW * kXStride;   // staged x
   p.Xs = o;   o += align16(MT * SW * 4); // per-column activation sums
   p.part = o; o += MT * SW * R * 4;      // per-entry partial products
-  p.tab = o;  o += tab_bytes;            // 1-bit lookup tables
+  if (tab_bytes > 0) o = (o + 255) & ~255;  // keeps every wave's tables 256-byte aligned
   p.bytes = o;
   return p;
 }
 
 // Whole workgroup: NW row-sum arrays (MT*R floats each), then NW regions.
-__host__ __device__ inline int mv_lds_bytes(int R, int SW, int MT, int NW, int tab_bytes = 0) {
-  return NW * (MT * R * 4 + wave_plan(R, SW, MT, tab_bytes).bytes);
+__host__ __device__ inline int mv_lds_bytes(int R, int SW, int MT, int NW, int tab_bytes = 0, bool index = true) {
+  return NW * (MT * R * 4 + wave_plan(R, SW, MT, tab_bytes, index).bytes);
 }
 
 // Group columns per width-map word (1 when a column spans whole words).
@@ -698,8 +700,29 @@ __device__ __forceinline__ void build_lut(int js, const Win& wn, uint32_t lane) 
 // decode_batch for one-width 1-bit windows of full tiles with R >= 64: slot i
 // of batch b is entries g0 .. g0 + 63, all in group column g0 / R, and the
 // slot that starts a column first builds its tables.
-__device__ __forceinline__ void decode_batch_lut(const Batch<0, 1>& bt, int n, int b, uint32_t lane,
-                                                 const Win& wn) {
+//
+// Table addresses: ta holds the tables' LDS base, which is 256-byte aligned,
+// so its low byte is zero.  One SDWA AND per lookup writes nibble*4 into that
+// byte and leaves the other three alone (dst_sel BYTE_0, UNUSED_PRESERVE),
+// and the table's own offset 64 m rides in the LDS instruction: one VALU
+// operation per lookup.  Byte k of w << 2, masked with 0x3C, is the low
+// nibble of byte k of w times 4; byte k of w >> 2 gives the high nibble.
+//
+// kRowAcc (R == 64 and a run of whole slots): lane l's entry of every slot is
+// row l, so each lane adds its slots' products to racc in column order (the
+// order the per-entry partials would be summed in), with no partial-product
+// store; otherwise the products go to the window's partial-product array.
+template <int K>
+__device__ __forceinline__ uint32_t lut_addr(uint32_t& ta, uint32_t shifted) {
+  __asm__("v_and_b32_sdwa %0, 60, %1 dst_sel:BYTE_0 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:BYTE_%2"
+          : "+v"(ta)
+          : "v"(shifted), "n"(K));
+  return ta;
+}
+
+template <bool kRowAcc>
+__device__ __forceinline__ void decode_batch_lut(const Batch<0, 1>& bt, int n, int b, uint32_t lane, const Win& wn,
+                                                 uint32_t (&ta)[4], float& racc) {
   constexpr int E = Batch<0, 1>::E;
 #pragma unroll
   for (int i = 0; i < E; ++i) {
@@ -713,28 +736,56 @@ __device__ __forceinline__ void decode_batch_lut(const Batch<0, 1>& bt, int n, i
       }
       const float X = lds_f32(wn.Xs + 4u * (uint32_t)js);
       const uint32_t w0 = bt.w[2 * i], w1 = bt.w[2 * i + 1];
-      // table m's entry for nibble m: one bit-field extract and one shift-add
-      // per lookup (written out: the compiler's shift, mask and add take three)
-      uint32_t tab_v;
-      __asm__("v_mov_b32 %0, %1" : "=v"(tab_v) : "s"(wn.tab));
+      const uint32_t sh[4] = {w0 << 2, w0 >> 2, w1 << 2, w1 >> 2};  // low / high nibbles of w0, w1
       float acc = 0.0f;
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
-        const uint32_t word = m < 8 ? w0 : w1;
+        // table m = 8 (word) + nibble; nibble n of a word is the low (n even)
+        // or high half of byte n >> 1
         uint32_t a;
-        __asm__("v_bfe_u32 %0, %1, %2, 4\n\tv_lshl_add_u32 %0, %0, 2, %3"
-                : "=&v"(a)
-                : "v"(word), "n"(4 * (m & 7)), "v"(tab_v));
+        const uint32_t v = sh[2 * (m >> 3) + (m & 1)];
+        switch ((m & 7) >> 1) {
+          case 0: a = lut_addr<0>(ta[m & 3], v); break;
+          case 1: a = lut_addr<1>(ta[m & 3], v); break;
+          case 2: a = lut_addr<2>(ta[m & 3], v); break;
+          default: a = lut_addr<3>(ta[m & 3], v); break;
+        }
         const float t = lds_f32(a + 64u * (uint32_t)m);
         acc = m == 0 ? t : acc + t;
       }
       const float s = (float)__builtin_bit_cast(_Float16, bt.s[i]);
-      // lanes past the end hold the run's last entry: same value, same place
-      const int p = min(g0 + (int)lane, n - 1);
-      lds_store_f32(wn.part + 4u * (uint32_t)p, s * __builtin_fmaf(acc, 2.0f, -X));
+      const float v = s * __builtin_fmaf(acc, 2.0f, -X);
+      if constexpr (kRowAcc) {
+        racc += v;  // every slot is full (n is a multiple of 64)
+      } else {
+        // lanes past the end hold the run's last entry: same value, same place
+        const int p = min(g0 + (int)lane, n - 1);
+        lds_store_f32(wn.part + 4u * (uint32_t)p, v);
+      }
       lds_phase();
     }
     __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// run_class for the lookup-table decode (same double-buffered loop).
+template <bool kRowAcc>
+__device__ __forceinline__ void run_lut(const DevMatrix& mat, Batch<0, 1>& A, uint32_t start, int n, const Win& wn,
+                                        uint32_t lane, float& racc) {
+  constexpr int per_batch = Batch<0, 1>::E * Batch<0, 1>::G;
+  const int nb = max(1, (n + per_batch - 1) / per_batch);
+  uint32_t ta[4] = {wn.tab, wn.tab, wn.tab, wn.tab};
+  if (nb == 1) {  // wave-uniform: no further batch, so no prefetch (each path keeps exact wait counts)
+    decode_batch_lut<kRowAcc>(A, n, 0, lane, wn, ta, racc);
+    return;
+  }
+  Batch<0, 1> B;
+  for (int b = 0; b < nb; b += 2) {
+    load_batch<0, 1>(B, mat, start, n, min(b + 1, nb - 1), lane);
+    decode_batch_lut<kRowAcc>(A, n, b, lane, wn, ta, racc);
+    if (b + 1 >= nb) break;
+    load_batch<0, 1>(A, mat, start, n, min(b + 2, nb - 1), lane);
+    decode_batch_lut<kRowAcc>(B, n, b + 1, lane, wn, ta, racc);
   }
 }
 
@@ -744,33 +795,23 @@ __device__ __forceinline__ void decode_batch_lut(const Batch<0, 1>& bt, int n, i
 // decoded.  The loop runs at least once and its loads are unconditional
 // (past the last batch they repeat it), so the count of outstanding loads
 // never depends on the data.
-// kLut: the 1-bit lookup-table decode (one-width 1-bit windows of full tiles
-// with R >= 64 only).
-template <int CLS, int MT, bool kUni, bool kLut>
-__device__ __forceinline__ void decode_any(const Batch<CLS, MT>& bt, uint32_t inv_c, int n, int b, uint32_t lane,
-                                           const Win& wn) {
-  if constexpr (kLut)
-    decode_batch_lut(bt, n, b, lane, wn);
-  else
-    decode_batch<CLS, MT, kUni>(bt, inv_c, n, b, lane, wn);
-}
 
-template <int CLS, int MT, bool kUni = false, bool kLut = false>
+template <int CLS, int MT, bool kUni = false>
 __device__ __forceinline__ void run_class(const DevMatrix& mat, Batch<CLS, MT>& A, uint32_t start, int n,
                                           uint32_t inv_c, const Win& wn, uint32_t lane) {
   constexpr int per_batch = Batch<CLS, MT>::E * Batch<CLS, MT>::G;
   const int nb = max(1, (n + per_batch - 1) / per_batch);
   if (MT == 1 && nb == 1) {  // wave-uniform: no further batch, so no prefetch (each path keeps exact wait counts)
-    decode_any<CLS, MT, kUni, kLut>(A, inv_c, n, 0, lane, wn);
+    decode_batch<CLS, MT, kUni>(A, inv_c, n, 0, lane, wn);
     return;
   }
   Batch<CLS, MT> B;
   for (int b = 0; b < nb; b += 2) {
     load_batch<CLS, MT>(B, mat, start, n, min(b + 1, nb - 1), lane);
-    decode_any<CLS, MT, kUni, kLut>(A, inv_c, n, b, lane, wn);
+    decode_batch<CLS, MT, kUni>(A, inv_c, n, b, lane, wn);
     if (b + 1 >= nb) break;
     load_batch<CLS, MT>(A, mat, start, n, min(b + 2, nb - 1), lane);
-    decode_any<CLS, MT, kUni, kLut>(B, inv_c, n, b + 1, lane, wn);
+    decode_batch<CLS, MT, kUni>(B, inv_c, n, b + 1, lane, wn);
   }
 }
 
@@ -932,7 +973,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
   const int wave = wave_id();
   const int t = blockIdx.x;  // one row tile per workgroup
   const int NS = MT * R;
-  const WavePlan P = wave_plan(R, SW, MT, UNI == 0 ? kLutBytes : 0);
+  const WavePlan P = wave_plan(R, SW, MT, UNI == 0 ? kLutBytes : 0, UNI < 0);
   const uint32_t ysum = lds0 + (uint32_t)(wave * NS * 4);
   const uint32_t region = lds0 + (uint32_t)(NW * NS * 4 + wave * P.bytes);
   Win wn;
@@ -968,10 +1009,27 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       load_batch<UNI, MT>(A, mat, first, n, 0, lane);
       store_x1(cols, xr, wn, lane);
       lds_phase();
-      if (UNI == 0 && MT == 1 && R >= 64 && u.rows == R)  // wave-uniform: slots of one column each
-        run_class<UNI, MT, true, UNI == 0 && MT == 1>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
-      else
+      if constexpr (UNI == 0 && MT == 1) {
+        // wave-uniform: lane l holds row l of every slot, and every slot is
+        // whole (a run cut short by a malformed blob takes the path below)
+        if (R == 64 && u.rows == 64 && n == cols * 64) {
+          float racc = 0.0f;
+          run_lut<true>(mat, A, first, n, wn, lane, racc);
+          lds_phase();
+          const uint32_t ya = ysum + 4u * lane;
+          lds_store_f32(ya, lds_f32(ya) + racc);
+          lds_phase();
+          continue;
+        }
+        if (R > 64 && u.rows == R) {  // wave-uniform: slots of one column each
+          float unused = 0.0f;
+          run_lut<false>(mat, A, first, n, wn, lane, unused);
+        } else {
+          run_class<UNI, MT, true>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
+        }
+      } else {
         run_class<UNI, MT, true>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
+      }
       lds_phase();
       reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
       lds_phase();
@@ -1801,8 +1859,9 @@ vbq_status launch_mv(const DevMatrix& m, uint32_t flags, const void* x, int64_t 
         ++classes;
       }
     if (classes == 1) {
-      // the 1-bit kernel holds one group column's lookup tables per wave
-      if (uni == 0) sh.lds = mv_lds_bytes(m.R, sh.SW, 1, sh.NW, kLutBytes);
+      // no position index; the 1-bit kernel holds one group column's lookup
+      // tables per wave
+      sh.lds = mv_lds_bytes(m.R, sh.SW, 1, sh.NW, uni == 0 ? kLutBytes : 0, false);
       if (sh.lds > kLdsLimit) return VBQ_ERR_UNSUPPORTED;
       switch (uni * 3 + (sh.NW == 4 ? 0 : sh.NW == 8 ? 1 : 2)) {
         case 0: return launch_mv_nw<1, 4, 0>(a, sh.lds, s);
