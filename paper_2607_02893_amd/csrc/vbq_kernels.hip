@@ -1010,9 +1010,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       store_x1(cols, xr, wn, lane);
       lds_phase();
       if constexpr (UNI == 0 && MT == 1) {
+        // the table addressing needs the tables on a 256-byte boundary (the
+        // dynamic LDS starts at 0 and the wave regions are multiples of 256
+        // bytes; should that ever not hold, the dot2 decode runs instead)
+        const bool tab_ok = (wn.tab & 255u) == 0u;
         // wave-uniform: lane l holds row l of every slot, and every slot is
         // whole (a run cut short by a malformed blob takes the path below)
-        if (R == 64 && u.rows == 64 && n == cols * 64) {
+        if (tab_ok && R == 64 && u.rows == 64 && n == cols * 64) {
           float racc = 0.0f;
           run_lut<true>(mat, A, first, n, wn, lane, racc);
           lds_phase();
@@ -1021,7 +1025,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
           lds_phase();
           continue;
         }
-        if (R > 64 && u.rows == R) {  // wave-uniform: slots of one column each
+        if (tab_ok && R > 64 && u.rows == R) {  // wave-uniform: slots of one column each
           float unused = 0.0f;
           run_lut<false>(mat, A, first, n, wn, lane, unused);
         } else {
