@@ -180,13 +180,17 @@ def _gen_pack(task):
     idx, cfg, seed, spec = task
     from paper_2607_02893_amd import synth, vbq
     bits, q, s = synth.make_matrix(spec, seed)
+    whole = None
     if spec.row_tiers is not None:
+        rb = vbq.pack_row_buckets(q, s, bits, n_threads=1)
         parts = [(rows, np.asarray(blob).copy(), bytes(d), algorithmic_bytes(bits[rows], len(rows), spec.K))
-                 for _, rows, blob, d in vbq.pack_row_buckets(q, s, bits, n_threads=1)]
+                 for _, rows, blob, d in rb]
+        # the whole blob, bucket table and row index: one vbq_gemv_buckets call
+        whole = (np.asarray(rb.blob).copy(), [bytes(b) for b in rb.buckets], rb.row_index.copy())
     else:
         blob, desc = vbq.pack_codes(q, s, bits, n_threads=1)
         parts = [(None, np.asarray(blob).copy(), bytes(desc), algorithmic_bytes(bits, spec.N, spec.K))]
-    return idx, parts, spec.N * spec.K
+    return idx, parts, spec.N * spec.K, whole
 
 
 def prepare(cfg, workers, uniform_bits=0, recipe=False):
@@ -579,7 +583,7 @@ def main():
     M = args.batch
     st = build_step(wl, packed, M, dev)
     del packed
-    log(f"{len(st.mats)} matrices in {len(st.launch_args)} launches, {st.total_w / 1e9:.2f}G weights, "
+    log(f"{len(st.mats)} matrices in {len(st.calls)} launches, {st.total_w / 1e9:.2f}G weights, "
         f"algorithmic {st.total_alg / 1e6:.1f} MB/step, blobs {st.blob_bytes / 1e6:.1f} MB")
     for _ in range(args.warmup):
         st.run(stream.cuda_stream)
@@ -672,7 +676,7 @@ def main():
     if not args.no_cpu:
         cpu = cpu_baseline(wl)
         log(f"cpu oracle: {cpu['value']} ms/step ({cpu['sample']})")
-    n_launch = len(st.launch_args)
+    n_launch = len(st.calls)
     out = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -798,22 +802,32 @@ def main_persistent(args, wl, st, stream):
 
 
 class Step:
-    """The launches of one decode step on device: per launch (desc, blob, x, y,
-    output-row map or 0, len(y)), its algorithmic bytes and kernel name."""
+    """The launches of one decode step on device.  launch_args: per GEMV (one per
+    bucket of a bucketed matrix) (desc, blob, x, y, output-row map or 0, len(y)),
+    what the one-launch step takes.  calls: the launches the step makes, each
+    ("gemv", launch_args index) or ("buckets", table, n, blob, row index, x, y,
+    len(y)) for a bucketed matrix in one vbq_gemv_buckets call; with each call's
+    algorithmic bytes, kernel name and shape label."""
 
     def __init__(self, M):
         self.M = M
         self.mats = []        # per matrix: ([(PackedMatrix, rows or None)], x, y, algorithmic bytes)
         self.launch_args = []
-        self.launch_alg = []
-        self.kernels = []
+        self.calls = []
+        self.launch_alg = []  # per call
+        self.kernels = []     # per call
+        self.labels = []      # per call
         self.total_alg = 0.0
         self.total_w = 0
         self.blob_bytes = 0
+        self._keep = []       # device buffers and ctypes tables the calls point at
 
     def launch(self, i, stream_ptr):
         from paper_2607_02893_amd import vbq
-        d, b, x, y, rows, ylen = self.launch_args[i]
+        c = self.calls[i]
+        if c[0] == "buckets":
+            return vbq.raw_gemv_buckets(*c[1:], stream_ptr)
+        d, b, x, y, rows, ylen = self.launch_args[c[1]]
         if rows:
             return vbq.raw_gemv_rows(d, b, x, y, ylen, rows, stream_ptr)
         if self.M == 1:
@@ -822,10 +836,10 @@ class Step:
 
     def run(self, stream_ptr, idx=None):
         from paper_2607_02893_amd import vbq
-        for i in (range(len(self.launch_args)) if idx is None else idx):
+        for i in (range(len(self.calls)) if idx is None else idx):
             r = self.launch(i, stream_ptr)
             if r != 0:
-                raise vbq.VbqError(r, "vbq_gemv / vbq_gemv_rows / vbq_gemm_small")
+                raise vbq.VbqError(r, "vbq_gemv / vbq_gemv_rows / vbq_gemv_buckets / vbq_gemm_small")
 
     def graph(self, stream, idx=None, reps=1):
         """The launches (all, or those in idx) captured as one HIP graph, reps
@@ -848,24 +862,46 @@ def build_step(wl, packed, M, dev):
     import torch
     from paper_2607_02893_amd import synth, vbq
     st = Step(M)
-    for idx, parts, nw in packed:
+    for idx, parts, nw, whole in packed:
         spec = wl.matrices[idx]
         xm = synth.make_x(spec, wl.seed, M)
         x = torch.from_numpy(np.ascontiguousarray(xm[0] if M == 1 else xm)).to(dev)
         y = torch.empty(spec.N if M == 1 else (M, spec.N), dtype=torch.float32, device=dev)
+        table = None
+        if whole is not None and M == 1:
+            blob_all = torch.from_numpy(whole[0]).to(dev)
+            rows_all = torch.from_numpy(whole[2]).to(dev)
+            bks = [vbq.VbqBucket.from_buffer_copy(b) for b in whole[1]]
+            if vbq.buckets_kernel_name(bks) != "per bucket":
+                table = (vbq.VbqBucket * vbq.MAX_BUCKETS)(*bks)
+                st._keep += [blob_all, rows_all, table]
         dev_parts, alg = [], 0.0
-        for rows, blob, dbytes, palg in parts:
+        for k, (rows, blob, dbytes, palg) in enumerate(parts):
             desc = vbq.VbqDesc.from_buffer_copy(dbytes)
-            Wp = vbq.PackedMatrix(blob, desc, device=dev)
-            rt = None if rows is None else torch.from_numpy(rows).to(dev)
+            if table is not None:  # the bucket's bytes and rows inside the whole buffers
+                off, r0 = int(table[k].blob_offset), int(table[k].row_begin)
+                Wp = vbq.PackedMatrix.on_device(blob_all[off:off + int(desc.total_bytes)], desc)
+                rt = rows_all[r0:r0 + len(rows)]
+            else:
+                Wp = vbq.PackedMatrix(blob, desc, device=dev)
+                rt = None if rows is None else torch.from_numpy(rows).to(dev)
             dev_parts.append((Wp, rt))
             palg += (2 * spec.K + 4 * desc.N) * (M - 1)  # x and y of the extra rows
             st.launch_args.append((desc, Wp.blob.data_ptr(), x.data_ptr(), y.data_ptr(),
                                    0 if rt is None else rt.data_ptr(), spec.N))
-            st.launch_alg.append(palg)
-            st.kernels.append(vbq.kernel_name(desc, M))
+            if table is None:
+                st.calls.append(("gemv", len(st.launch_args) - 1))
+                st.launch_alg.append(palg)
+                st.kernels.append(vbq.kernel_name(desc, M))
+                st.labels.append(f"{desc.N}x{desc.K}" + (" (row bucket)" if rt is not None else ""))
             alg += palg
             st.blob_bytes += desc.total_bytes
+        if table is not None:
+            st.calls.append(("buckets", table, len(parts), blob_all.data_ptr(), rows_all.data_ptr(),
+                             x.data_ptr(), y.data_ptr(), spec.N))
+            st.launch_alg.append(alg)
+            st.kernels.append(vbq.buckets_kernel_name(list(table)[:len(parts)]))
+            st.labels.append(f"{spec.N}x{spec.K} ({len(parts)} row buckets, one launch)")
         st.mats.append((dev_parts, x, y, alg))
         st.total_alg += alg
         st.total_w += nw
@@ -942,7 +978,7 @@ def per_kernel_timing(st, stream, steps, warmup):
 def per_shape_timing(st, stream, n_ev):
     """Diagnostic: each launch bracketed by its own events (adds event overhead)."""
     import torch
-    n = len(st.launch_args)
+    n = len(st.calls)
     starts = [[torch.cuda.Event(enable_timing=True) for _ in range(n)] for _ in range(n_ev)]
     ends = [[torch.cuda.Event(enable_timing=True) for _ in range(n)] for _ in range(n_ev)]
     for r in range(n_ev):
@@ -954,8 +990,8 @@ def per_shape_timing(st, stream, n_ev):
     dur = np.median(np.array([[starts[r][i].elapsed_time(ends[r][i]) * 1e-3 for i in range(n)]
                               for r in range(n_ev)]), axis=0)
     per = {}
-    for i, la in enumerate(st.launch_args):
-        key = f"{la[0].N}x{la[0].K}" + (" (row bucket)" if la[4] else "")
+    for i in range(n):
+        key = st.labels[i]
         e = per.setdefault(key, {"count": 0, "us": [], "alg_bytes": st.launch_alg[i], "kernel": st.kernels[i]})
         e["count"] += 1
         e["us"].append(1e6 * dur[i])
@@ -1010,14 +1046,14 @@ def small_workload(cfg, args, dev, stream, flush):
     wl, packed = prepare(cfg, args.workers)
     st = build_step(wl, packed, 1, dev)
     g = st.graph(stream)
-    reps = -(-512 // len(st.launch_args))  # hot: the step repeated in one graph, >= 512 launches
+    reps = -(-512 // len(st.calls))  # hot: the step repeated in one graph, >= 512 launches
     gr = st.graph(stream, reps=reps)
     for _ in range(max(5, args.warmup)):
         gr.replay()
     _, hot_gpu = timed(gr.replay, max(10, args.steps // reps), stream)
     hot_gpu /= reps
     cold = cold_steps(g.replay, max(20, min(100, args.steps)), flush, stream)
-    out = {"name": wl.name, "launches": len(st.launch_args), "algorithmic_bytes": int(st.total_alg),
+    out = {"name": wl.name, "launches": len(st.calls), "algorithmic_bytes": int(st.total_alg),
            "hot_us": round(1e6 * hot_gpu, 2),
            "hot_timing": f"HIP events around replays of a graph holding the step {reps} times in a row",
            "cold_us": cold,

@@ -262,12 +262,20 @@ vbq_status vbq_pack_row_buckets(int64_t N, int64_t K, const int8_t* q,
                                 vbq_bucket buckets[VBQ_MAX_BUCKETS],
                                 int32_t* n_buckets, int32_t* row_index);
 
-/* y = w_hat x for a bucketed matrix: vbq_gemv_rows for each bucket in turn on
- * one stream, bucket i reading blob_dev + buckets[i].blob_offset and writing
- * rows row_index_dev[row_begin ..].  The bucket descriptors' flags apply.
- * blob_dev 256-byte aligned; row_index_dev device int32[sum n_rows]; y_dev
- * device float32[y_len] (fp16 with VBQ_Y_F16).  Errors: as vbq_gemv_rows, and
- * SHAPE for n_buckets outside [0, VBQ_MAX_BUCKETS]. */
+/* y = w_hat x for a bucketed matrix (paper section 6, the head stored as
+ * frequency-grouped row buckets): bucket i reads blob_dev +
+ * buckets[i].blob_offset and writes its rows to y[row_index_dev[row_begin +
+ * n]], each row's value bit for bit that of vbq_gemv_rows on the bucket.
+ * When two or more buckets each take the four-wave one-width kernel and all
+ * carry the same flags (as vbq_pack_row_buckets' buckets of one call do),
+ * every bucket runs in ONE launch (vbq_buckets_kernel<4>, the buckets side
+ * by side); otherwise vbq_gemv_rows runs for each bucket in turn on the
+ * stream.  The buckets' output rows must not overlap (with one launch, which
+ * bucket's value lands in a shared row is unspecified).  The bucket
+ * descriptors' flags apply.  blob_dev 256-byte aligned; row_index_dev device
+ * int32[sum n_rows]; y_dev device float32[y_len] (fp16 with VBQ_Y_F16).
+ * Errors: as vbq_gemv_rows, and SHAPE for n_buckets outside
+ * [0, VBQ_MAX_BUCKETS]. */
 vbq_status vbq_gemv_buckets(const vbq_bucket* buckets, int32_t n_buckets,
                             const void* blob_dev, const int32_t* row_index_dev,
                             const void* x_dev, void* y_dev, int64_t y_len,
@@ -365,6 +373,12 @@ vbq_status vbq_step_run_noalloc(const void* plan_dev, int32_t n, uint32_t spin_l
  * or M outside [1, 16]).  The choice depends on the widths present, the grid
  * and the flags; a caller or a profile can group launches by it. */
 const char* vbq_kernel_name(const vbq_desc* desc, int64_t M);
+
+/* What vbq_gemv_buckets launches for these buckets: "vbq_buckets_kernel<4>"
+ * (one launch for all of them), "per bucket" (vbq_gemv_rows for each; see
+ * vbq_kernel_name) or "none" (n_buckets outside [1, VBQ_MAX_BUCKETS] or
+ * NULL).  Static storage; only the descriptors are looked at. */
+const char* vbq_gemv_buckets_kernel_name(const vbq_bucket* buckets, int32_t n_buckets);
 
 /* W_dev[n][k] = w_hat[n][k] = s*q as float32 (exact), device float32[N][K].
  * For checking the packed stream against the quantizer bit for bit. */

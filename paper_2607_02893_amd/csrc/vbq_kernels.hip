@@ -27,6 +27,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 #include <cstdint>
@@ -923,6 +924,91 @@ __device__ __forceinline__ int clamp_run(const DevMatrix& mat, int c, uint32_t s
   return start >= lim ? 0 : (int)min(n, lim - start);
 }
 
+// One row tile of a one-width matrix (class UNI, one activation row): the
+// workgroup's NW waves take the tile's items (unit slices) in turn, decode
+// them and add their row sums, then the workgroup adds the waves' sums and
+// writes the tile's rows.  Every group has width class UNI, so entries sit at
+// consecutive real positions: no width map, no class counts, no index, and a
+// unit's first entry follows from the geometry.  Shared by vbq_mv_kernel and
+// the all-buckets kernel.
+template <int NW, int UNI>
+__device__ __forceinline__ void uniform_tile(const DevMatrix& mat, const MvArgs& a, int t, int S, int SW) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int R = mat.R;
+  const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
+  const uint32_t lane = lane_id();
+  const int wave = wave_id();
+  const WavePlan P = wave_plan(R, SW, 1, UNI == 0 ? kLutBytes : 0, false);
+  const uint32_t ysum = lds0 + (uint32_t)(wave * R * 4);
+  const uint32_t region = lds0 + (uint32_t)(NW * R * 4 + wave * P.bytes);
+  Win wn;
+  wn.xs = region + P.xs;
+  wn.Xs = region + P.Xs;
+  wn.part = region + P.part;
+  wn.tab = region + P.tab;
+  wn.xstride_m = (uint32_t)(SW * kXStride);
+  wn.part_m = (uint32_t)(SW * R * 4);
+  wn.SW = SW;
+  wn.logR = mat.logR;
+  for (int i = (int)lane; i < R; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
+
+  for (int item = wave; item < mat.U * S; item += NW) {
+    const uint32_t lane = lane_id_here();
+    const int k = item / S, sl = item - k * S;
+    const UnitInfo u = load_unit(mat, t, k);
+    int cb, ce;
+    slice_cols(u.cols, R, sl, S, cb, ce);
+    if (cb >= ce) continue;  // wave-uniform: an empty slice
+    XRegs xr;
+    load_x1(a.x, u.j0 + cb, ce - cb, xr, lane);
+    // all tiles above this one are full: R*G entries each; this tile's units
+    // hold C*rows entries each
+    const uint32_t first = (uint32_t)t * (uint32_t)(R * mat.G) + (uint32_t)(u.j0 + cb) * (uint32_t)u.rows;
+    const int cols = ce - cb;
+    const int n = clamp_run(mat, UNI, first, (uint32_t)(cols * u.rows));
+    Batch<UNI, 1> A;
+    load_batch<UNI, 1>(A, mat, first, n, 0, lane);
+    store_x1(cols, xr, wn, lane);
+    lds_phase();
+    if constexpr (UNI == 0) {
+      // the table addressing needs the tables on a 256-byte boundary (the
+      // dynamic LDS starts at 0 and the wave regions are multiples of 256
+      // bytes; should that ever not hold, the dot2 decode runs instead)
+      const bool tab_ok = (wn.tab & 255u) == 0u;
+      // wave-uniform: lane l holds row l of every slot, and every slot is
+      // whole (a run cut short by a malformed blob takes the path below)
+      if (tab_ok && R == 64 && u.rows == 64 && n == cols * 64) {
+        float racc = 0.0f;
+        run_lut<true>(mat, A, first, n, wn, lane, racc);
+        lds_phase();
+        const uint32_t ya = ysum + 4u * lane;
+        lds_store_f32(ya, lds_f32(ya) + racc);
+        lds_phase();
+        continue;
+      }
+      if (tab_ok && R > 64 && u.rows == R) {  // wave-uniform: slots of one column each
+        float unused = 0.0f;
+        run_lut<false>(mat, A, first, n, wn, lane, unused);
+      } else {
+        run_class<UNI, 1, true>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
+      }
+    } else {
+      run_class<UNI, 1, true>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
+    }
+    lds_phase();
+    reduce_window<1>(wn, R, cols, u.rows, ysum, lane);
+    lds_phase();
+  }
+  __syncthreads();
+  const int rows = min(R, mat.N - t * R);
+  for (int r = threadIdx.x; r < rows; r += NW * 64) {
+    float tot = 0.0f;
+#pragma unroll
+    for (int w2 = 0; w2 < NW; ++w2) tot += lds_f32(lds0 + 4u * (uint32_t)(w2 * R + r));
+    store_row(a, (size_t)t * R + r, tot);
+  }
+}
+
 // One activation row keeps 4 waves per SIMD (at most 128 VGPRs); more rows
 // trade occupancy for registers.
 //
@@ -968,167 +1054,180 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
   a.x = x;
   a.M = (int)(sw_m >> 16);
   const int R = mat.R, SW = (int)(sw_m & 0xFFFF), S = (int)(geo >> 21);
-  const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
-  const uint32_t lane = lane_id();
-  const int wave = wave_id();
-  const int t = blockIdx.x;  // one row tile per workgroup
-  const int NS = MT * R;
-  const WavePlan P = wave_plan(R, SW, MT, UNI == 0 ? kLutBytes : 0, UNI < 0);
-  const uint32_t ysum = lds0 + (uint32_t)(wave * NS * 4);
-  const uint32_t region = lds0 + (uint32_t)(NW * NS * 4 + wave * P.bytes);
-  Win wn;
-  wn.xs = region + P.xs;
-  wn.Xs = region + P.Xs;
-  wn.part = region + P.part;
-  wn.tab = region + P.tab;
-  wn.xstride_m = (uint32_t)(SW * kXStride);
-  wn.part_m = (uint32_t)(SW * R * 4);
-  wn.SW = SW;
-  wn.logR = mat.logR;
-  const uint32_t inv = region + P.inv;
-  for (int i = (int)lane; i < NS; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
+  if constexpr (UNI >= 0) {
+    static_assert(MT == 1, "one-width matrices take one activation row");
+    uniform_tile<NW, UNI>(mat, a, blockIdx.x, S, SW);  // one row tile per workgroup
+  } else {
+    const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
+    const uint32_t lane = lane_id();
+    const int wave = wave_id();
+    const int t = blockIdx.x;  // one row tile per workgroup
+    const int NS = MT * R;
+    const WavePlan P = wave_plan(R, SW, MT);
+    const uint32_t ysum = lds0 + (uint32_t)(wave * NS * 4);
+    const uint32_t region = lds0 + (uint32_t)(NW * NS * 4 + wave * P.bytes);
+    Win wn;
+    wn.xs = region + P.xs;
+    wn.Xs = region + P.Xs;
+    wn.part = region + P.part;
+    wn.tab = region + P.tab;
+    wn.xstride_m = (uint32_t)(SW * kXStride);
+    wn.part_m = (uint32_t)(SW * R * 4);
+    wn.SW = SW;
+    wn.logR = mat.logR;
+    const uint32_t inv = region + P.inv;
+    for (int i = (int)lane; i < NS; i += 64) lds_store_f32(ysum + 4u * i, 0.0f);
 
-  for (int item = wave; item < mat.U * S; item += NW) {
-    const uint32_t lane = lane_id_here();
-    const int k = item / S, sl = item - k * S;
-    const UnitInfo u = load_unit(mat, t, k);
-    const int unit = t * mat.U + k;
-    int cb, ce;
-    slice_cols(u.cols, R, sl, S, cb, ce);
-    if (cb >= ce) continue;  // wave-uniform: an empty slice
-    const int slice_we = (ce * R + 63) >> 6;
-    XRegs xr;
-    if constexpr (MT == 1) load_x1(a.x, u.j0 + cb, ce - cb, xr, lane);  // with the map: one latency
-    if constexpr (UNI >= 0) {
-      // all tiles above this one are full: R*G entries each; this tile's
-      // units hold C*rows entries each
-      const uint32_t first = (uint32_t)t * (uint32_t)(R * mat.G) + (uint32_t)(u.j0 + cb) * (uint32_t)u.rows;
-      const int cols = ce - cb;
-      const int n = clamp_run(mat, UNI, first, (uint32_t)(cols * u.rows));
-      Batch<UNI, MT> A;
-      load_batch<UNI, MT>(A, mat, first, n, 0, lane);
-      store_x1(cols, xr, wn, lane);
+    for (int item = wave; item < mat.U * S; item += NW) {
+      const uint32_t lane = lane_id_here();
+      const int k = item / S, sl = item - k * S;
+      const UnitInfo u = load_unit(mat, t, k);
+      const int unit = t * mat.U + k;
+      int cb, ce;
+      slice_cols(u.cols, R, sl, S, cb, ce);
+      if (cb >= ce) continue;  // wave-uniform: an empty slice
+      const int slice_we = (ce * R + 63) >> 6;
+      XRegs xr;
+      if constexpr (MT == 1) load_x1(a.x, u.j0 + cb, ce - cb, xr, lane);  // with the map: one latency
+      // A whole-unit item (one slice per unit) reads where its class runs start
+      // and how long they are from the unit table (rows u and u + 1): no class
+      // counts, and its code loads do not wait for the width map.
+      const bool whole = MT == 1 && S == 1;  // wave-uniform
+      const u32x16 rows2 = unit_rows(mat, unit);
+      const u32x4 erow = rows2.s0123, enext = rows2.s89ab;
+      const uint32_t ustart[4] = {erow.x, erow.y, erow.z, erow.w};
+      const WmapRegs wr = load_wmap(mat, u, slice_we, lane);
+      // The class sections' offsets and sizes come from the kernel-argument
+      // block (not preloaded): read them only now, so that the loads above do
+      // not wait for that block (it would otherwise be read, and waited for,
+      // before the work loop).
       lds_phase();
-      if constexpr (UNI == 0 && MT == 1) {
-        // the table addressing needs the tables on a 256-byte boundary (the
-        // dynamic LDS starts at 0 and the wave regions are multiples of 256
-        // bytes; should that ever not hold, the dot2 decode runs instead)
-        const bool tab_ok = (wn.tab & 255u) == 0u;
-        // wave-uniform: lane l holds row l of every slot, and every slot is
-        // whole (a run cut short by a malformed blob takes the path below)
-        if (tab_ok && R == 64 && u.rows == 64 && n == cols * 64) {
-          float racc = 0.0f;
-          run_lut<true>(mat, A, first, n, wn, lane, racc);
-          lds_phase();
-          const uint32_t ya = ysum + 4u * lane;
-          lds_store_f32(ya, lds_f32(ya) + racc);
-          lds_phase();
-          continue;
-        }
-        if (tab_ok && R > 64 && u.rows == R) {  // wave-uniform: slots of one column each
-          float unused = 0.0f;
-          run_lut<false>(mat, A, first, n, wn, lane, unused);
-        } else {
-          run_class<UNI, MT, true>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
-        }
-      } else {
-        run_class<UNI, MT, true>(mat, A, first, n, (uint32_t)u.rows, wn, lane);
-      }
-      lds_phase();
-      reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
-      lds_phase();
-      continue;
-    }
-    // A whole-unit item (one slice per unit) reads where its class runs start
-    // and how long they are from the unit table (rows u and u + 1): no class
-    // counts, and its code loads do not wait for the width map.
-    const bool whole = MT == 1 && S == 1;  // wave-uniform
-    const u32x16 rows2 = unit_rows(mat, unit);
-    const u32x4 erow = rows2.s0123, enext = rows2.s89ab;
-    const uint32_t ustart[4] = {erow.x, erow.y, erow.z, erow.w};
-    const WmapRegs wr = load_wmap(mat, u, slice_we, lane);
-    // The class sections' offsets and sizes come from the kernel-argument
-    // block (not preloaded): read them only now, so that the loads above do
-    // not wait for that block (it would otherwise be read, and waited for,
-    // before the work loop).
-    lds_phase();
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      mat.off_codes[c] = opaque(mat.off_codes[c]);
-      mat.off_scales[c] = opaque(mat.off_scales[c]);
-      mat.n_entries[c] = opaque(mat.n_entries[c]);
-    }
-    auto window = [&](int c0, int c1) __attribute__((always_inline)) {
-      const int cols = c1 - c0;
-      const int wb = (c0 * R) >> 6, we = (c1 * R + 63) >> 6;
-      const bool unit_window = whole && c0 == cb && c1 == ce;  // wave-uniform
-      WinCounts wc;
-      if (unit_window) {
-        const u32x4 own = enext - erow;
-        wc.own[0] = own.x;
-        wc.own[1] = own.y;
-        wc.own[2] = own.z;
-        wc.own[3] = own.w;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) wc.before[c] = 0u;
-      } else {
-        wc = window_counts(wr, u, wb, we, R, lane);
-      }
-      XRegs xrm[MT > 1 ? MT : 1];
-      if constexpr (MT > 1) load_xm<MT>(a, u.j0 + c0, cols, xrm, lane);  // (several rows: per window)
-      uint32_t start[4], seg[4];
-      int n[4];
-      uint32_t o = 0;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        start[c] = ustart[c] + wc.before[c];
-        n[c] = clamp_run(mat, c, start[c], wc.own[c]);
-        seg[c] = inv + 2u * o;
-        o += wc.own[c];
+        mat.off_codes[c] = opaque(mat.off_codes[c]);
+        mat.off_scales[c] = opaque(mat.off_scales[c]);
+        mat.n_entries[c] = opaque(mat.n_entries[c]);
       }
-      // the first batch of every class is in flight while x is stored and the
-      // index is built (and, for several rows, x is staged): one memory
-      // latency for all four
-      Batch<0, MT> A0;
-      Batch<1, MT> A1;
-      Batch<2, MT> A2;
-      Batch<3, MT> A3;
-      load_batch<0, MT>(A0, mat, start[0], n[0], 0, lane);
-      load_batch<1, MT>(A1, mat, start[1], n[1], 0, lane);
-      load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
-      load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
-      // one row: x arrived with the map and goes to LDS now
-      if constexpr (MT == 1) store_x1(cols, xr, wn, lane);
-      build_index(wr, u, wb, we, R, wc, inv, lane);
-      if constexpr (MT > 1) store_xm<MT>(a, cols, xrm, wn, lane);
-      lds_phase();
-      run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
-      run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
-      run_class<2, MT>(mat, A2, start[2], n[2], seg[2], wn, lane);
-      run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
-      lds_phase();
-      reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
-      lds_phase();
-    };
-    if constexpr (MT == 1) {
-      window(cb, ce);  // one row: the window is the whole slice
-    } else {
-      for (int c0 = cb; c0 < ce; c0 += SW) window(c0, min(ce, c0 + SW));
+      auto window = [&](int c0, int c1) __attribute__((always_inline)) {
+        const int cols = c1 - c0;
+        const int wb = (c0 * R) >> 6, we = (c1 * R + 63) >> 6;
+        const bool unit_window = whole && c0 == cb && c1 == ce;  // wave-uniform
+        WinCounts wc;
+        if (unit_window) {
+          const u32x4 own = enext - erow;
+          wc.own[0] = own.x;
+          wc.own[1] = own.y;
+          wc.own[2] = own.z;
+          wc.own[3] = own.w;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) wc.before[c] = 0u;
+        } else {
+          wc = window_counts(wr, u, wb, we, R, lane);
+        }
+        XRegs xrm[MT > 1 ? MT : 1];
+        if constexpr (MT > 1) load_xm<MT>(a, u.j0 + c0, cols, xrm, lane);  // (several rows: per window)
+        uint32_t start[4], seg[4];
+        int n[4];
+        uint32_t o = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          start[c] = ustart[c] + wc.before[c];
+          n[c] = clamp_run(mat, c, start[c], wc.own[c]);
+          seg[c] = inv + 2u * o;
+          o += wc.own[c];
+        }
+        // the first batch of every class is in flight while x is stored and the
+        // index is built (and, for several rows, x is staged): one memory
+        // latency for all four
+        Batch<0, MT> A0;
+        Batch<1, MT> A1;
+        Batch<2, MT> A2;
+        Batch<3, MT> A3;
+        load_batch<0, MT>(A0, mat, start[0], n[0], 0, lane);
+        load_batch<1, MT>(A1, mat, start[1], n[1], 0, lane);
+        load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
+        load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
+        // one row: x arrived with the map and goes to LDS now
+        if constexpr (MT == 1) store_x1(cols, xr, wn, lane);
+        build_index(wr, u, wb, we, R, wc, inv, lane);
+        if constexpr (MT > 1) store_xm<MT>(a, cols, xrm, wn, lane);
+        lds_phase();
+        run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
+        run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
+        run_class<2, MT>(mat, A2, start[2], n[2], seg[2], wn, lane);
+        run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
+        lds_phase();
+        reduce_window<MT>(wn, R, cols, u.rows, ysum, lane);
+        lds_phase();
+      };
+      if constexpr (MT == 1) {
+        window(cb, ce);  // one row: the window is the whole slice
+      } else {
+        for (int c0 = cb; c0 < ce; c0 += SW) window(c0, min(ce, c0 + SW));
+      }
+    }
+    __syncthreads();
+    const int rows = min(R, mat.N - t * R);
+    for (int slot = threadIdx.x; slot < NS; slot += NW * 64) {
+      const int m = slot >> mat.logR, r = slot & (R - 1);
+      if (m < a.M && r < rows) {
+        float tot = 0.0f;
+#pragma unroll
+        for (int w2 = 0; w2 < NW; ++w2) tot += lds_f32(lds0 + 4u * (uint32_t)(w2 * NS + slot));
+        if (MT == 1)
+          store_row(a, (size_t)t * R + r, tot);
+        else
+          store_y(a.y, m * a.ldy + (size_t)t * R + r, tot, a.yf16);
+      }
     }
   }
-  __syncthreads();
-  const int rows = min(R, mat.N - t * R);
-  for (int slot = threadIdx.x; slot < NS; slot += NW * 64) {
-    const int m = slot >> mat.logR, r = slot & (R - 1);
-    if (m < a.M && r < rows) {
-      float tot = 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// Every row bucket of a bucketed matrix in one launch (one-width buckets, one
+// activation row).  Workgroups [tile0[b], tile0[b + 1]) take bucket b's row
+// tiles; each runs uniform_tile for its bucket's width class, so a tile's
+// arithmetic is that of the bucket's own vbq_gemv_rows launch.  The buckets
+// run side by side instead of one after another.
+// ---------------------------------------------------------------------------
+struct BucketsArgs {
+  DevMatrix m[VBQ_MAX_BUCKETS];
+  const int32_t* rows[VBQ_MAX_BUCKETS];  // output row of each bucket row
+  int32_t tile0[VBQ_MAX_BUCKETS];        // first workgroup of each bucket
+  int32_t cls[VBQ_MAX_BUCKETS];          // width class (log2 bits)
+  int32_t S[VBQ_MAX_BUCKETS];            // slices per unit
+  int32_t SW[VBQ_MAX_BUCKETS];           // window columns
+  int32_t n;                             // buckets
+  int32_t yf16;
+  const uint16_t* x;
+  void* y;
+  int64_t ylen;
+};
+
+template <int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) void vbq_buckets_kernel(BucketsArgs ba) {
+  int b = 0;
 #pragma unroll
-      for (int w2 = 0; w2 < NW; ++w2) tot += lds_f32(lds0 + 4u * (uint32_t)(w2 * NS + slot));
-      if (MT == 1)
-        store_row(a, (size_t)t * R + r, tot);
-      else
-        store_y(a.y, m * a.ldy + (size_t)t * R + r, tot, a.yf16);
-    }
+  for (int i = 1; i < VBQ_MAX_BUCKETS; ++i)
+    if (i < ba.n && (int)blockIdx.x >= ba.tile0[i]) b = i;
+  MvArgs a;
+  a.m = ba.m[b];
+  a.x = ba.x;
+  a.y = ba.y;
+  a.ldx = 0;
+  a.ldy = 0;
+  a.M = 1;
+  a.S = ba.S[b];
+  a.SW = ba.SW[b];
+  a.yf16 = ba.yf16;
+  a.rows = ba.rows[b];
+  a.ylen = ba.ylen;
+  const int t = (int)blockIdx.x - ba.tile0[b];
+  switch (ba.cls[b]) {
+    case 0: uniform_tile<NW, 0>(a.m, a, t, a.S, a.SW); break;
+    case 1: uniform_tile<NW, 1>(a.m, a, t, a.S, a.SW); break;
+    case 2: uniform_tile<NW, 2>(a.m, a, t, a.S, a.SW); break;
+    default: uniform_tile<NW, 3>(a.m, a, t, a.S, a.SW); break;
   }
 }
 
@@ -1956,6 +2055,53 @@ vbq_status launch_mm(const DevMatrix& m, uint32_t flags, const void* x, int64_t 
 
 // Name of the kernel a product with M activation rows launches on this matrix
 // (the same choices as launch_mv / launch_mm); static storage.
+// The one-launch plan of a bucketed GEMV (vbq_buckets_kernel<4>): every bucket
+// a one-width matrix that the four-wave one-width kernel takes, two or more
+// buckets, all with the same call options, every bucket's blob 256-byte
+// aligned.  Buckets go smallest first, so their few tiles are dispatched
+// with the first wave of workgroups.  False when the buckets do not qualify.
+bool plan_buckets(const vbq_bucket* bk, int n, const void* blob, const int32_t* rows, BucketsArgs* ba, int* grid,
+                  int* lds) {
+  if (n < 2 || n > VBQ_MAX_BUCKETS) return false;
+  int order[VBQ_MAX_BUCKETS];
+  DevMatrix ms[VBQ_MAX_BUCKETS];
+  for (int i = 0; i < n; ++i) {
+    if (bk[i].desc.flags != bk[0].desc.flags || bk[i].row_begin < 0 || bk[i].n_rows != bk[i].desc.N) return false;
+    if (make_dev_matrix(&bk[i].desc, (const uint8_t*)blob + bk[i].blob_offset, &ms[i]) != VBQ_OK) return false;
+    order[i] = i;
+  }
+  std::sort(order, order + n, [&](int p, int q) { return ms[p].T != ms[q].T ? ms[p].T < ms[q].T : p < q; });
+  *ba = BucketsArgs{};
+  int tiles = 0, need = 0;
+  for (int k = 0; k < n; ++k) {
+    const int i = order[k];
+    const DevMatrix& m = ms[i];
+    int uni = -1, classes = 0;
+    for (int c = 0; c < 4; ++c)
+      if (m.n_entries[c]) {
+        uni = c;
+        ++classes;
+      }
+    MvShape sh;
+    if (classes != 1 || !choose_shape(m, 1, &sh) || sh.NW != 4) return false;
+    need = std::max(need, mv_lds_bytes(m.R, sh.SW, 1, 4, uni == 0 ? kLutBytes : 0, false));
+    ba->m[k] = m;
+    ba->rows[k] = rows + bk[i].row_begin;
+    ba->tile0[k] = tiles;
+    ba->cls[k] = uni;
+    ba->S[k] = sh.S;
+    ba->SW[k] = sh.SW;
+    if ((int64_t)tiles + m.T > INT32_MAX) return false;
+    tiles += (int)m.T;
+  }
+  if (need > kLdsLimit) return false;
+  ba->n = n;
+  ba->yf16 = (bk[0].desc.flags & VBQ_Y_F16) ? 1 : 0;
+  *grid = tiles;
+  *lds = need;
+  return true;
+}
+
 const char* kernel_name(const DevMatrix& m, uint32_t flags, int M) {
   // (template arguments as the compiler prints them, spaces removed; the
   // uniform kernel's last argument is the width class log2 b)
@@ -2332,11 +2478,44 @@ vbq_status vbq_gemv_buckets(const vbq_bucket* buckets, int32_t n_buckets, const 
   for (int32_t i = 0; i < n_buckets; ++i) {
     const vbq_bucket& b = buckets[i];
     if (b.row_begin < 0 || b.n_rows != b.desc.N) return VBQ_ERR_DESC;
+  }
+  if (x_dev && y_dev && y_len >= 0 && (uintptr_t)x_dev % 16 == 0 && (uintptr_t)row_index_dev % 4 == 0) {
+    BucketsArgs ba;
+    int grid = 0, lds = 0;
+    if (plan_buckets(buckets, n_buckets, blob_dev, row_index_dev, &ba, &grid, &lds) &&
+        (uintptr_t)y_dev % y_align(&buckets[0].desc) == 0) {
+      ba.x = (const uint16_t*)x_dev;
+      ba.y = y_dev;
+      ba.ylen = y_len;
+      const void* kernel = (const void*)vbq_buckets_kernel<4>;
+      if (lds > 64 * 1024) {
+        static std::atomic<uint64_t> done{0};
+        vbq_status st = allow_big_lds(kernel, done);
+        if (st != VBQ_OK) return st;
+      }
+      void* kargs[] = {&ba};
+      return hip_status(hipLaunchKernel(kernel, dim3((unsigned)grid), dim3(4 * 64), kargs, (size_t)lds,
+                                        (hipStream_t)stream));
+    }
+  }
+  // otherwise (and for every argument error) one vbq_gemv_rows per bucket
+  for (int32_t i = 0; i < n_buckets; ++i) {
+    const vbq_bucket& b = buckets[i];
     const vbq_status st = vbq_gemv_rows(&b.desc, (const uint8_t*)blob_dev + b.blob_offset, x_dev, y_dev, y_len,
                                         row_index_dev + b.row_begin, stream);
     if (st != VBQ_OK) return st;
   }
   return VBQ_OK;
+}
+
+const char* vbq_gemv_buckets_kernel_name(const vbq_bucket* buckets, int32_t n_buckets) {
+  if (n_buckets < 1 || n_buckets > VBQ_MAX_BUCKETS || !buckets) return "none";
+  BucketsArgs ba;
+  int grid = 0, lds = 0;
+  // (any aligned non-null addresses: only the descriptors are looked at)
+  if (plan_buckets(buckets, n_buckets, (const void*)(uintptr_t)256, (const int32_t*)(uintptr_t)256, &ba, &grid, &lds))
+    return "vbq_buckets_kernel<4>";
+  return "per bucket";
 }
 
 vbq_status vbq_gemm_small(const vbq_desc* desc, const void* blob_dev, int64_t M, const void* X_dev, int64_t ldx,

@@ -57,7 +57,8 @@ STATUS = {0: "VBQ_OK", 1: "VBQ_ERR_NULL", 2: "VBQ_ERR_SHAPE", 3: "VBQ_ERR_BITS",
 EXPORTS = ("vbq_status_string", "vbq_last_hip_error", "vbq_layout_version", "vbq_pack_size", "vbq_pack", "vbq_pack_codes",
            "vbq_desc_check", "vbq_gemv", "vbq_gemv_rows", "vbq_pack_row_buckets_size", "vbq_pack_row_buckets",
            "vbq_gemv_buckets", "vbq_gemm_small", "vbq_step_plan_bytes", "vbq_step_workspace_bytes",
-           "vbq_step_plan", "vbq_step_run", "vbq_step_run_noalloc", "vbq_kernel_name", "vbq_dequant",
+           "vbq_step_plan", "vbq_step_run", "vbq_step_run_noalloc", "vbq_kernel_name", "vbq_gemv_buckets_kernel_name",
+           "vbq_dequant",
            "vbq_qat_workspace_size", "vbq_qat_forward", "vbq_qat_logit_grad", "vbq_read_ceiling")
 # vbq_desc.flags (call options)
 Y_F16 = 1
@@ -146,6 +147,8 @@ _lib.vbq_step_run_noalloc.restype = ctypes.c_int
 _lib.vbq_step_run_noalloc.argtypes = [_P, ctypes.c_int32, ctypes.c_uint32, _P, _P]
 _lib.vbq_kernel_name.restype = ctypes.c_char_p
 _lib.vbq_kernel_name.argtypes = [ctypes.POINTER(VbqDesc), ctypes.c_int64]
+_lib.vbq_gemv_buckets_kernel_name.restype = ctypes.c_char_p
+_lib.vbq_gemv_buckets_kernel_name.argtypes = [ctypes.POINTER(VbqBucket), ctypes.c_int32]
 _lib.vbq_read_ceiling.restype = ctypes.c_int
 _lib.vbq_read_ceiling.argtypes = [_P, ctypes.c_size_t, ctypes.c_uint32, _P, _P]
 _lib.vbq_dequant.restype = ctypes.c_int
@@ -273,7 +276,23 @@ def pack_row_buckets(q, scales, bits, tile_rows=0, chunk_groups=0, n_threads=0):
         d = VbqDesc.from_buffer_copy(b.desc)
         out.append((int(b.bits), row_index[b.row_begin:b.row_begin + n].copy(),
                     blob[off:off + int(d.total_bytes)], d))
-    return out
+    return RowBuckets(out, blob, bk, row_index)
+
+
+class RowBuckets(list):
+    """pack_row_buckets' result: [(width, rows, blob, desc)] per bucket, plus the
+    whole blob, the bucket table and the row index as vbq_pack_row_buckets wrote
+    them (what vbq_gemv_buckets takes)."""
+
+    def __init__(self, items, blob, buckets, row_index):
+        super().__init__(items)
+        self.blob, self.buckets, self.row_index = blob, buckets, row_index
+
+
+def buckets_kernel_name(buckets):
+    """vbq_gemv_buckets_kernel_name for a list of VbqBucket."""
+    table = (VbqBucket * max(1, len(buckets)))(*buckets)
+    return _lib.vbq_gemv_buckets_kernel_name(table, len(buckets)).decode()
 
 
 def desc_check(d):
@@ -370,6 +389,18 @@ class PackedMatrix:
         if self.blob.data_ptr() % 256:
             raise VbqError(7, "PackedMatrix")
 
+    @classmethod
+    def on_device(cls, blob, desc):
+        """A packed matrix whose bytes are already in device memory (a uint8 tensor,
+        e.g. one bucket's slice of a bucketed blob), 256-byte aligned."""
+        self = cls.__new__(cls)
+        self.desc = desc
+        self.N, self.K = desc.N, desc.K
+        self.blob = blob
+        if blob.data_ptr() % 256:
+            raise VbqError(7, "PackedMatrix")
+        return self
+
     @property
     def nbytes(self):
         return int(self.desc.total_bytes)
@@ -454,13 +485,27 @@ class PackedMatrix:
 
 class BucketedMatrix:
     """A row-bucketed matrix in device memory: one PackedMatrix per width and
-    the output rows of its members (see pack_row_buckets)."""
+    the output rows of its members (see pack_row_buckets).  From a RowBuckets
+    the whole blob and row index go to the device as one buffer each, and gemv
+    is one vbq_gemv_buckets call."""
 
     def __init__(self, buckets, N, K, device="cuda"):
         import torch
         self.N, self.K = N, K
-        self.parts = [(b, PackedMatrix(blob, d, device), torch.from_numpy(rows).to(device))
-                      for b, rows, blob, d in buckets]
+        self.table = None
+        if isinstance(buckets, RowBuckets):
+            self.blob = torch.from_numpy(np.asarray(buckets.blob, dtype=np.uint8)).to(device)
+            self.row_index = torch.from_numpy(np.ascontiguousarray(buckets.row_index)).to(device)
+            self.table = (VbqBucket * MAX_BUCKETS)(*buckets.buckets)
+            self.n_buckets = len(buckets.buckets)
+            self.parts = []
+            for (b, _, _, d), bk in zip(buckets, buckets.buckets):
+                off, r0, n = int(bk.blob_offset), int(bk.row_begin), int(bk.n_rows)
+                part = PackedMatrix.on_device(self.blob[off:off + int(d.total_bytes)], d)
+                self.parts.append((b, part, self.row_index[r0:r0 + n]))
+        else:
+            self.parts = [(b, PackedMatrix(blob, d, device), torch.from_numpy(rows).to(device))
+                          for b, rows, blob, d in buckets]
         if sum(p[1].N for p in self.parts) != N:
             raise ValueError("the buckets must hold every row once")
 
@@ -468,9 +513,25 @@ class BucketedMatrix:
     def nbytes(self):
         return sum(p[1].nbytes for p in self.parts)
 
+    def kernel_name(self):
+        """What gemv launches (vbq_gemv_buckets_kernel_name), or "per bucket"."""
+        if self.table is None:
+            return "per bucket"
+        return _lib.vbq_gemv_buckets_kernel_name(self.table, self.n_buckets).decode()
+
+    def call_table(self, y_dtype):
+        """A copy of the bucket table with the fp16-output option set or cleared."""
+        import torch
+        t = (VbqBucket * MAX_BUCKETS)()
+        ctypes.memmove(t, self.table, ctypes.sizeof(t))
+        for i in range(self.n_buckets):
+            t[i].desc.flags = Y_F16 if y_dtype == torch.float16 else 0
+        return t
+
     def gemv(self, x, y=None, stream=None):
-        """y[N] = w_hat @ x: one vbq_gemv_rows per bucket, on one stream; y float32
-        (or a given float16 tensor)."""
+        """y[N] = w_hat @ x; y float32 (or a given float16 tensor).  One
+        vbq_gemv_buckets call (from a RowBuckets), else one vbq_gemv_rows per
+        bucket, on one stream."""
         import torch
         dev = self.parts[0][1].blob.device
         if y is None:
@@ -478,9 +539,23 @@ class BucketedMatrix:
         if y.dtype not in (torch.float32, torch.float16):
             raise ValueError("y must be float32 or float16")
         _need(y, "y", y.dtype, self.N, dev)
+        if self.table is not None:
+            _need(x, "x", torch.float16, self.K, dev)
+            _check(_lib.vbq_gemv_buckets(self.call_table(y.dtype), self.n_buckets,
+                                         ctypes.c_void_p(self.blob.data_ptr()),
+                                         ctypes.c_void_p(self.row_index.data_ptr()), ctypes.c_void_p(x.data_ptr()),
+                                         ctypes.c_void_p(y.data_ptr()), y.numel(), _stream_handle(stream)),
+                   "vbq_gemv_buckets")
+            return y
         for _, Wp, rows in self.parts:
             Wp.gemv_rows(x, y, rows, stream)
         return y
+
+
+def raw_gemv_buckets(table, n_buckets, blob_ptr, row_index_ptr, x_ptr, y_ptr, y_len, stream_ptr):
+    """vbq_gemv_buckets with raw device addresses (a ctypes VbqBucket array)."""
+    return _lib.vbq_gemv_buckets(table, n_buckets, ctypes.c_void_p(blob_ptr), ctypes.c_void_p(row_index_ptr),
+                                 ctypes.c_void_p(x_ptr), ctypes.c_void_p(y_ptr), y_len, ctypes.c_void_p(stream_ptr))
 
 
 # ------------------------------------------------- differentiable bit selection

@@ -376,6 +376,52 @@ def test_row_buckets_match_oracle(vbq, N, K):
     _say(f"  max rel err {rel:.2e}")
 
 
+@pytest.mark.parametrize("N,K,tiers", [(3000, 1024, None), (100, 640, None), (128256, 4096, None),
+                                        (700, 4096, ((0.5, 1), (0.5, 8))), (5000, 2048, ((0.9, 2), (0.1, 4)))])
+def test_buckets_one_launch_bitwise_per_bucket(vbq, N, K, tiers):
+    """vbq_gemv_buckets runs every row bucket in one launch (vbq_buckets_kernel<4>):
+    bit for bit the per-bucket vbq_gemv_rows launches, fp32 and fp16 outputs,
+    including buckets of a single partial tile (100 rows over four widths)."""
+    spec = synth.MatrixSpec("h", 0, 4, N, K, row_tiers=tiers or synth.RECIPE_HEAD_TIERS)
+    bits, q, s = synth.make_matrix(spec, 211)
+    x = _x_dev(synth.make_x(spec, 211)[0])
+    rb = vbq.pack_row_buckets(q, s, bits)
+    one = vbq.BucketedMatrix(rb, N, K)
+    each = vbq.BucketedMatrix(list(rb), N, K)
+    assert one.kernel_name() == "vbq_buckets_kernel<4>" and each.kernel_name() == "per bucket"
+    _say(f"buckets N={N} K={K}: {[(b, p.N, p.desc.tile_rows) for b, p, _ in one.parts]}")
+    for dt in (torch.float32, torch.float16):
+        y1 = torch.full((N,), float("nan"), dtype=dt, device="cuda")
+        y2 = torch.full((N,), float("nan"), dtype=dt, device="cuda")
+        one.gemv(x, y1)
+        each.gemv(x, y2)
+        torch.cuda.synchronize()
+        assert torch.isfinite(y1.float()).all(), dt
+        assert torch.equal(y1, y2), dt
+    if N <= 5000:
+        y = one.gemv(x).cpu().numpy()
+        xh = synth.make_x(spec, 211)[0]
+        parity.check(y, omatmul.gemv(q, s, xh), omatmul.row_magnitude(q, s, xh), what=f"one-launch buckets {N}x{K}")
+
+
+def test_buckets_one_launch_short_y(vbq):
+    """Rows whose output index is past y_len are skipped in the one-launch path
+    as in vbq_gemv_rows (a y of the first 1000 rows of a 3000-row head)."""
+    N, K = 3000, 1024
+    spec = synth.MatrixSpec("h", 0, 4, N, K, row_tiers=synth.RECIPE_HEAD_TIERS)
+    bits, q, s = synth.make_matrix(spec, 223)
+    x = _x_dev(synth.make_x(spec, 223)[0])
+    one = vbq.BucketedMatrix(vbq.pack_row_buckets(q, s, bits), N, K)
+    full = one.gemv(x)
+    y = torch.full((1008,), -5.0, dtype=torch.float32, device="cuda")
+    st = vbq.raw_gemv_buckets(one.call_table(torch.float32), one.n_buckets, one.blob.data_ptr(),
+                              one.row_index.data_ptr(), x.data_ptr(), y.data_ptr(), 1000, 0)
+    assert st == 0
+    torch.cuda.synchronize()
+    assert torch.equal(y[:1000], full[:1000])
+    assert torch.all(y[1000:] == -5.0)
+
+
 def test_recipe_workload_full_size(vbq):
     """The 9B-class recipe step at full size: uniform 2- and 4-bit projections
     (the one-width kernel) and the tiered LM head as row buckets, sampled rows

@@ -284,6 +284,27 @@ def test_pack_row_buckets_c_abi():
     assert lib.vbq_gemv_buckets(out, 1, None, None, None, None, 0, None) == 1
 
 
+def test_buckets_kernel_choice():
+    """vbq_gemv_buckets_kernel_name (descriptors only): a tiered head's buckets
+    take one launch; one bucket, buckets whose one-width kernel would use more
+    than four waves (K = 16384: eight units per tile), or buckets with unequal
+    flags take one vbq_gemv_rows each; no bucket is "none"."""
+    spec = synth.MatrixSpec("h", 0, 4, 3000, 1024, row_tiers=synth.RECIPE_HEAD_TIERS)
+    bits, q, s = synth.make_matrix(spec, 61)
+    rb = vbq.pack_row_buckets(q, s, bits)
+    assert len(rb.buckets) == 4
+    assert vbq.buckets_kernel_name(rb.buckets) == "vbq_buckets_kernel<4>"
+    assert vbq.buckets_kernel_name(rb.buckets[:2]) == "vbq_buckets_kernel<4>"
+    assert vbq.buckets_kernel_name(rb.buckets[:1]) == "per bucket"
+    assert vbq.buckets_kernel_name([]) == "none"
+    mixed = [vbq.VbqBucket.from_buffer_copy(b) for b in rb.buckets]
+    mixed[1].desc.flags = vbq.Y_F16
+    assert vbq.buckets_kernel_name(mixed) == "per bucket"
+    wide = synth.MatrixSpec("w", 0, 4, 200, 16384, row_tiers=((0.5, 1), (0.5, 2)))
+    bits, q, s = synth.make_matrix(wide, 67)
+    assert vbq.buckets_kernel_name(vbq.pack_row_buckets(q, s, bits).buckets) == "per bucket"
+
+
 def test_step_plan_argument_errors():
     """vbq_step_plan / _bytes / _run check everything on the host first."""
     lib = vbq.lib()
