@@ -1237,11 +1237,20 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
 // With one wave per unit a small matrix leaves each SIMD one or two waves,
 // and every wave runs its index build and its four class runs one after the
 // other, each a chain of LDS round trips.  Here a pair of waves shares the
-// unit: role 0 loads the width map, builds the index and decodes the 1-bit
-// run; role 1 loads x, stages it and decodes the 2-, 4- and 8-bit runs.
+// unit: role 0 loads the width map, builds the index and decodes the 1- and
+// 8-bit runs; role 1 loads x, stages it and decodes the 2- and 4-bit runs.
 // Both read the unit's class runs from the unit table (rows u and u + 1), so
 // both issue their first code loads at once.  Workgroup barriers separate
 // the set-up, the decode and the row reduction.
+//
+// A wave's class runs follow one another, and every run after the first
+// batch waits on memory for each further batch (a run of a few batches of
+// short decodes hides little of that wait), so what bounds a role is mostly
+// its number of batches.  A unit's short runs (2-, 4- and 8-bit, about two
+// batches each) therefore go two to role 1 and one to role 0, beside the
+// long 1-bit run whose decode covers its own next loads: measured against
+// all three on role 1, the 9B-class step took 1075-1080 us instead of 1102,
+// the 1.46B-class step 682 instead of 723 us.
 //
 // The roles do unequal VALU work (the 1-bit run is most of the entries), and
 // a workgroup's waves are dealt to the CU's four SIMDs in turn, so with pairs
@@ -1346,11 +1355,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
     }
     if (role == 0) {
       load_batch<0, MT>(A0, mat, start[0], n[0], 0, lane);
+      load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
       build_index(wr, u, 0, u.W, R, wc, inv, lane);
     } else {
       load_batch<1, MT>(A1, mat, start[1], n[1], 0, lane);
       load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
-      load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
       if constexpr (MT == 1)
         store_x1(u.cols, xr, wn, lane);
       else
@@ -1361,10 +1370,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
   if (active) {
     if (role == 0) {
       run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
+      run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
     } else {
       run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
       run_class<2, MT>(mat, A2, start[2], n[2], seg[2], wn, lane);
-      run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
     }
   }
   __syncthreads();  // every partial product is in LDS
