@@ -1870,8 +1870,7 @@ vbq_status launch_mv_nw(const MvArgs& a, int lds, hipStream_t s) {
 
 // Wave pairs: one or two rows, mixed widths, whole units of at most 32
 // columns, at most 8 units per tile (4 for two rows), and a grid small enough
-// that one wave per unit would leave the SIMDs with at most two waves each
-// (half as large for two rows).
+// that one wave per unit would leave the SIMDs with at most two waves each.
 constexpr int kPairMaxUnits = 2048;
 
 template <int NW, int MT>
@@ -1894,16 +1893,13 @@ vbq_status launch_pair_nw(const MvArgs& a, int lds, hipStream_t s) {
   return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
 }
 
-// Launches the pair kernel for MT (1 or 2) activation rows when the matrix
-// qualifies; *used says whether it did.
-// Waves per workgroup of the pair kernel for MT activation rows, or 0 when
-// the matrix does not qualify.
+// Waves per workgroup of the pair kernel for MT (1 or 2) activation rows, or
+// 0 when the matrix does not qualify.
 int pair_waves(const DevMatrix& m, int MT) {
   int classes = 0;
   for (int c = 0; c < 4; ++c) classes += m.n_entries[c] ? 1 : 0;
   if (classes < 2 || m.U < 2 || m.U > 8 || m.C > kXRegs * 8) return 0;
-  // (two rows: a grid half as large, beyond which the one-wave kernel is faster)
-  if ((int64_t)m.T * m.U > (MT == 1 ? kPairMaxUnits : kPairMaxUnits / 2)) return 0;
+  if ((int64_t)m.T * m.U > kPairMaxUnits) return 0;
   // two rows fit the registers of 8 waves per workgroup (2 per SIMD), not of 16
   if (MT > 1 && m.U > 4) return 0;
   const int NW = m.U <= 4 ? 8 : 16;
@@ -1911,6 +1907,8 @@ int pair_waves(const DevMatrix& m, int MT) {
   return lds > kLdsLimit ? 0 : NW;
 }
 
+// Launches the pair kernel for MT (1 or 2) activation rows when the matrix
+// qualifies; *used says whether it did.
 template <int MT>
 vbq_status try_launch_pair(const DevMatrix& m, const void* x, int64_t ldx, void* y, int64_t ldy, bool yf16,
                            const int32_t* rows, int64_t ylen, hipStream_t s, bool* used) {

@@ -191,15 +191,16 @@ def test_exact_probes_bucketed_head(vbq):
 
 # several activation rows: X rows are probes and random rows, every row of Y checked
 BATCH = [
-    ("o", 2, "pair kernel, two rows (256 tiles x 4 units)"),
-    ("qkv", 2, "one wave per unit, two rows (1536 units)"),
-    ("gate_up", 4, "matrix cores, 64-row tiles"),
-    ("down", 16, "matrix cores, 16-row tiles, 8 units"),
+    ("o", 2, "pair kernel, two rows (256 tiles x 4 units)", False),
+    ("qkv", 2, "pair kernel, two rows (1536 units)", False),
+    ("qkv", 2, "one wave per unit, two rows (1536 units)", True),
+    ("gate_up", 4, "matrix cores, 64-row tiles", False),
+    ("down", 16, "matrix cores, 16-row tiles, 8 units", False),
 ]
 
 
-@pytest.mark.parametrize("name,M,kernel", BATCH)
-def test_exact_probes_9b_batch(vbq, name, M, kernel):
+@pytest.mark.parametrize("name,M,kernel,one_wave", BATCH)
+def test_exact_probes_9b_batch(vbq, name, M, kernel, one_wave):
     wl = synth.workload(3)
     spec = _spec(wl, name)
     _say(f"9B {name} {spec.N}x{spec.K} M={M}: {kernel}")
@@ -214,7 +215,10 @@ def test_exact_probes_9b_batch(vbq, name, M, kernel):
     X[0, k0] = 1.0                        # row 0: one-hot
     X[1] = 0
     X[1, 64 * j0:64 * j0 + 64] = 1.0      # row 1: group sum
-    Y = Wp.gemm_small(_dev(X)).cpu().numpy()
+    if M == 2:
+        want = "vbq_mv_kernel<2,4>" if one_wave else "vbq_mv_pair_kernel<8,2>"
+        assert vbq.kernel_name(Wp.call_desc(one_wave_per_unit=one_wave), M) == want
+    Y = Wp.gemm_small(_dev(X), one_wave_per_unit=one_wave).cpu().numpy()
     assert np.array_equal(Y[0].astype(np.float64), _column(q, s, k0)), "one-hot row"
     assert np.array_equal(Y[1].astype(np.float64), _group_sum(q, s, j0)), "group-sum row"
     worst_rel, worst_b = 0.0, 0.0
@@ -223,7 +227,7 @@ def test_exact_probes_9b_batch(vbq, name, M, kernel):
         worst_rel = max(worst_rel, parity.check(Y[m], ystar, _row_mag(q, s, X[m]), what=f"{name} M={M} row {m}"))
         worst_b = max(worst_b, parity.check_bound(Y[m], ystar, parity.fp32_bound(q, s, bits, X[m]),
                                                   what=f"{name} M={M} row {m}"))
-    Y16 = Wp.gemm_small(_dev(X), y_dtype=torch.float16).cpu().numpy()
+    Y16 = Wp.gemm_small(_dev(X), y_dtype=torch.float16, one_wave_per_unit=one_wave).cpu().numpy()
     assert np.array_equal(Y16.view(np.uint16), Y.astype(np.float16).view(np.uint16)), "fp16 output"
     _say(f"9B {name} M={M}: exact rows ok; max rel err {worst_rel:.2e}, max err / float32 bound {worst_b:.3f}")
 
