@@ -1487,7 +1487,7 @@ struct MmBlock {
 // Block f of the row group: column f / RB, row block rg*RB + f % RB.  The
 // lane's levels 16h .. 16h + 15 (h = lane / 16) are pairs 8h .. 8h + 7, whose
 // codes start at byte (2h << c) & ~3 of the entry.  Loads are unconditional
-// (clamped), so several blocks stay in flight.  X comes through a buffer
+// (clamped), so the next block stays in flight.  X comes through a buffer
 // resource (xr) covering the M rows.
 template <int RB>
 __device__ __forceinline__ void load_mm_block(MmBlock& bk, __amdgpu_buffer_rsrc_t xr, int64_t ldx, int M,
@@ -1631,28 +1631,27 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
       float4_t acc[RB];
 #pragma unroll
       for (int i = 0; i < RB; ++i) acc[i] = float4_t{0.0f, 0.0f, 0.0f, 0.0f};
-      MmBlock B0, B1, B2, B3;
+      // two blocks in flight (the next one loads while one is multiplied):
+      // with four, every wave's chain of index lookups and loads got longer
+      // (1.46B-class step at M = 4: 1415 against 1262 us); block f adds into
+      // acc[f % RB] (the ring slot)
+      MmBlock B0, B1;
       load_mm_block<RB>(B0, xr, ldx, M, mat, fwd, tab, 0, rg, rows, j0, lane);
-      load_mm_block<RB>(B1, xr, ldx, M, mat, fwd, tab, min(1, last), rg, rows, j0, lane);
-      load_mm_block<RB>(B2, xr, ldx, M, mat, fwd, tab, min(2, last), rg, rows, j0, lane);
-      // four blocks in flight; block f adds into acc[f % RB] (the ring slot)
       for (int f = 0; f < nf; f += 4) {
-        load_mm_block<RB>(B3, xr, ldx, M, mat, fwd, tab, min(f + 3, last), rg, rows, j0, lane);
+        load_mm_block<RB>(B1, xr, ldx, M, mat, fwd, tab, min(f + 1, last), rg, rows, j0, lane);
         acc[0 % RB] += mm_products(B0);
         mm_done(B0);
-        load_mm_block<RB>(B0, xr, ldx, M, mat, fwd, tab, min(f + 4, last), rg, rows, j0, lane);
+        load_mm_block<RB>(B0, xr, ldx, M, mat, fwd, tab, min(f + 2, last), rg, rows, j0, lane);
         if (f + 1 < nf) acc[1 % RB] += mm_products(B1);
         mm_done(B1);
-        load_mm_block<RB>(B1, xr, ldx, M, mat, fwd, tab, min(f + 5, last), rg, rows, j0, lane);
-        if (f + 2 < nf) acc[2 % RB] += mm_products(B2);
-        mm_done(B2);
-        load_mm_block<RB>(B2, xr, ldx, M, mat, fwd, tab, min(f + 6, last), rg, rows, j0, lane);
-        if (f + 3 < nf) acc[3 % RB] += mm_products(B3);
-        mm_done(B3);
+        load_mm_block<RB>(B1, xr, ldx, M, mat, fwd, tab, min(f + 3, last), rg, rows, j0, lane);
+        if (f + 2 < nf) acc[2 % RB] += mm_products(B0);
+        mm_done(B0);
+        load_mm_block<RB>(B0, xr, ldx, M, mat, fwd, tab, min(f + 4, last), rg, rows, j0, lane);
+        if (f + 3 < nf) acc[3 % RB] += mm_products(B1);
+        mm_done(B1);
       }
       mm_done(B0);
-      mm_done(B1);
-      mm_done(B2);
       // this wave's share of the row sums (several items add up in order)
 #pragma unroll
       for (int i = 0; i < RB; ++i) {
