@@ -1136,24 +1136,26 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
           seg[c] = inv + 2u * o;
           o += wc.own[c];
         }
-        // the first batch of every class is in flight while x is stored and the
-        // index is built (and, for several rows, x is staged): one memory
-        // latency for all four
+        // the 1- and 2-bit runs' first batches are in flight while x is stored
+        // and the index is built (and, for several rows, x is staged); the 4-
+        // and 8-bit runs' first batches go out one run ahead of their decode
+        // (all four at once made every wave's chain longer: the 9B-class LM
+        // head took 40.6-41.3 us against 39.7-39.9, at 128 VGPRs against 107)
         Batch<0, MT> A0;
         Batch<1, MT> A1;
         Batch<2, MT> A2;
         Batch<3, MT> A3;
         load_batch<0, MT>(A0, mat, start[0], n[0], 0, lane);
         load_batch<1, MT>(A1, mat, start[1], n[1], 0, lane);
-        load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
-        load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
         // one row: x arrived with the map and goes to LDS now
         if constexpr (MT == 1) store_x1(cols, xr, wn, lane);
         build_index(wr, u, wb, we, R, wc, inv, lane);
         if constexpr (MT > 1) store_xm<MT>(a, cols, xrm, wn, lane);
         lds_phase();
         run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
+        load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
         run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
+        load_batch<3, MT>(A3, mat, start[3], n[3], 0, lane);
         run_class<2, MT>(mat, A2, start[2], n[2], seg[2], wn, lane);
         run_class<3, MT>(mat, A3, start[3], n[3], seg[3], wn, lane);
         lds_phase();
