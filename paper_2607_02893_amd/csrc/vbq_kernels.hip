@@ -1633,11 +1633,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
       float4_t acc[RB];
 #pragma unroll
       for (int i = 0; i < RB; ++i) acc[i] = float4_t{0.0f, 0.0f, 0.0f, 0.0f};
-      // two blocks in flight (the next one loads while one is multiplied):
+      // Two blocks in flight (the next one loads while one is multiplied):
       // with four, every wave's chain of index lookups and loads got longer
-      // (1.46B-class step at M = 4: 1415 against 1262 us); block f adds into
-      // acc[f % RB] (the ring slot)
+      // (1.46B-class step at M = 4: 1415 against 1262 us).  With more than
+      // four rows of X, tiles of one or four row blocks take one block at a
+      // time (their blocks read more X; at M = 16 the step took 1551 against
+      // 1603 us, at M = 4 it would take 1281 against 1264).  Block f adds
+      // into acc[f % RB] (the ring slot) either way.
       MmBlock B0, B1;
+      if (RB != 2 && M > 4) {  // wave-uniform
+        for (int f = 0; f < nf; ++f) {
+          load_mm_block<RB>(B0, xr, ldx, M, mat, fwd, tab, f, rg, rows, j0, lane);
+          acc[f % RB] += mm_products(B0);
+          mm_done(B0);
+        }
+      } else {
       load_mm_block<RB>(B0, xr, ldx, M, mat, fwd, tab, 0, rg, rows, j0, lane);
       for (int f = 0; f < nf; f += 4) {
         load_mm_block<RB>(B1, xr, ldx, M, mat, fwd, tab, min(f + 1, last), rg, rows, j0, lane);
@@ -1654,6 +1664,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
         mm_done(B1);
       }
       mm_done(B0);
+      }
       // this wave's share of the row sums (several items add up in order)
 #pragma unroll
       for (int i = 0; i < RB; ++i) {
