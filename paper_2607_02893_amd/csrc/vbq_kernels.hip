@@ -509,18 +509,22 @@ __device__ __forceinline__ void build_index(const WmapRegs& wr, const UnitInfo& 
 }
 
 // ---------------------------------------------------------------------------
-// Batches.  Every lane holds 32 bytes of codes per batch: E = 4, 2, 1 whole
-// entries for widths 1, 2, 4, and half an entry for width 8 with one
-// activation row (L = 2 lanes per entry: lanes 2j and 2j+1 hold the low and
-// high halves of one entry; several rows take whole 8-bit entries).  Slot
-// i of batch b covers the run's entries (bE + i) * 64/L .. + 64/L - 1, one per
-// lane (or lane pair), so every load instruction reads one contiguous span.
+// Batches.  Every lane holds 32 bytes of codes per batch for widths 2, 4 and
+// 8: E = 2 and 1 whole entries for widths 2 and 4, and half an entry for
+// width 8 with one activation row (L = 2 lanes per entry: lanes 2j and 2j+1
+// hold the low and high halves of one entry; several rows take whole 8-bit
+// entries).  Width 1 takes E = 2 entries (16 bytes): with four (32 bytes) a
+// wave keeps more bytes in flight, and every kernel got slower (the 9B-class
+// step 1045 against 1070 us, the one-width 1-bit 1.46B-class step 557 against
+// 570 us; one entry was slower again, 1058 and 603 us).  Slot i of batch b
+// covers the run's entries (bE + i) * 64/L .. + 64/L - 1, one per lane (or
+// lane pair), so every load instruction reads one contiguous span.
 // ---------------------------------------------------------------------------
 template <int CLS, int MT>
 struct Batch {
   static constexpr int NW = 2 << CLS;                    // uint32 words per entry
   static constexpr int L = CLS == 3 && MT == 1 ? 2 : 1;  // lanes per entry
-  static constexpr int E = CLS == 3 ? 1 : 4 >> CLS;     // entry slots per lane
+  static constexpr int E = CLS == 3 ? 1 : CLS == 0 ? 2 : 4 >> CLS;  // entry slots per lane
   static constexpr int LW = NW / L;                // words per lane per slot
   static constexpr int G = 64 / L;                 // entries per slot across the wave
   uint32_t w[E * LW];
