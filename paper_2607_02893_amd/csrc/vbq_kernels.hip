@@ -1592,7 +1592,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
   mat.R = (int)(geo & 0x1FF);
   mat.C = (int)((geo >> 9) & 0xFF);
   mat.logR = (int)((geo >> 17) & 0xF);
-  const int R = mat.R, S = (int)(geo >> 21);
+  const int R = mat.R, S = (int)((geo >> 21) & 0x3FF);
+  const bool setup_prio = (geo >> 31) != 0u;  // raised issue priority for each item's set-up
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem;
   const int wave = wave_id();
   const int t = blockIdx.x;  // one row tile per workgroup
@@ -1615,6 +1616,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
     int cb, ce;
     slice_cols(u.cols, R, sl, S, cb, ce);
     if (cb >= ce) continue;  // wave-uniform: an empty slice
+    if (setup_prio) __builtin_amdgcn_s_setprio(1);
     const int wb = (cb * R) >> 6, we = (ce * R + 63) >> 6;
     const WmapRegs wr = load_wmap(mat, u, we, lane);
     const u32x16 rows2 = unit_rows(mat, unit);  // beside the width map, not after it
@@ -1642,6 +1644,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
 #undef VBQ_MM_ROW
     build_index<true>(wr, u, wb, we, R, wc, fwd, lane);
     lds_phase();
+    if (setup_prio) __builtin_amdgcn_s_setprio(0);
     const int j0 = u.j0 + cb;
     const int nf = (ce - cb) * RB;  // blocks per row group
     const int last = nf - 1;
@@ -2039,7 +2042,11 @@ vbq_status launch_mm_nw(const MmArgs& a, int lds, hipStream_t s) {
   uint32_t off_wmap = a.m.off_wmap, tile_words = a.m.tile_words, chunk_words = a.m.chunk_words;
   uint32_t wmap_words = a.m.wmap_words;
   int32_t G = a.m.G, N = a.m.N, U = a.m.U;
-  uint32_t geo = (uint32_t)a.m.R | ((uint32_t)a.m.C << 9) | ((uint32_t)a.m.logR << 17) | ((uint32_t)a.S << 21);
+  // bit 31: each item's set-up (width map, class runs, index) at a raised issue
+  // priority, for up to eight rows (1.46B-class step: M = 4 1271 -> 1260 us, M = 8
+  // 1343 -> 1326 us; at M = 16 it was slower, 1548 -> 1555 us)
+  uint32_t geo = (uint32_t)a.m.R | ((uint32_t)a.m.C << 9) | ((uint32_t)a.m.logR << 17) | ((uint32_t)a.S << 21) |
+                 (a.M <= 8 ? 1u << 31 : 0u);
   void* kargs[] = {&blob, &off_wmap, &tile_words, &chunk_words, &wmap_words, &G, &N, &geo, &U, &args};
   return hip_status(hipLaunchKernel(kernel, dim3((unsigned)a.m.T), dim3(NW * 64), kargs, (size_t)lds, s));
 }
