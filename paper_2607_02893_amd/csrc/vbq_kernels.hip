@@ -1090,11 +1090,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       int cb, ce;
       slice_cols(u.cols, R, sl, S, cb, ce);
       if (cb >= ce) continue;  // wave-uniform: an empty slice
-      // one row: a wave's set-up (x, the map, the first code loads and the
-      // index) runs at a raised issue priority, so a wave that has just
+      // one or two rows: a wave's set-up (x, the map, the first code loads and
+      // the index) runs at a raised issue priority, so a wave that has just
       // started gets its loads out ahead of the decode of the waves around it
-      // (9B-class LM head: 38.8 -> 37.7 us a launch in the step)
-      if (MT == 1) __builtin_amdgcn_s_setprio(1);
+      // (9B-class LM head: 38.8 -> 37.7 us a launch in the step; two rows:
+      // 72.2 -> 71.0 us, the 9B-class down 17.6 -> 17.4 us)
+      if (MT <= 2) __builtin_amdgcn_s_setprio(1);
       const int slice_we = (ce * R + 63) >> 6;
       XRegs xr;
       if constexpr (MT == 1) load_x1(a.x, u.j0 + cb, ce - cb, xr, lane);  // with the map: one latency
@@ -1161,7 +1162,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
         build_index(wr, u, wb, we, R, wc, inv, lane);
         if constexpr (MT > 1) store_xm<MT>(a, cols, xrm, wn, lane);
         lds_phase();
-        if (MT == 1) __builtin_amdgcn_s_setprio(0);
+        if (MT <= 2) __builtin_amdgcn_s_setprio(0);
         run_class<0, MT>(mat, A0, start[0], n[0], seg[0], wn, lane);
         load_batch<2, MT>(A2, mat, start[2], n[2], 0, lane);
         run_class<1, MT>(mat, A1, start[1], n[1], seg[1], wn, lane);
