@@ -921,6 +921,21 @@ __device__ __forceinline__ u32x16 unit_rows(const DevMatrix& mat, int unit) {
   return ld<u32x16>(mat.blob, 4u * (uint32_t)unit * vbq::kUnitRowWords);
 }
 
+// The same two rows read through the vector memory path (lane l reads word
+// l & 15, then the 16 words are moved to scalar registers).  Measured against
+// the scalar load: faster in the matrix-core kernel (1.46B-class M = 4: Q|K|V
+// 7.74 -> 7.50 us a launch) and in the 16-wave pair kernel (9B-class down
+// 8.37 -> 8.19 us), slower in the 8-wave pair kernel (1.46B-class step 660 ->
+// 675 us), so only those two use it.
+__device__ __forceinline__ u32x16 unit_rows_vec(const DevMatrix& mat, int unit) {
+  const uint32_t l = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)) & 15u;
+  const uint32_t v = ld<uint32_t>(mat.blob, 4u * ((uint32_t)unit * vbq::kUnitRowWords + l));
+  u32x16 r;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) r[i] = __builtin_amdgcn_readlane(v, i);
+  return r;
+}
+
 // Entries of a run that stay inside the class section (a malformed blob can
 // make the width map and the unit table disagree).
 __device__ __forceinline__ int clamp_run(const DevMatrix& mat, int c, uint32_t start, uint32_t n) {
@@ -1346,7 +1361,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1
       load_x1(x, u.j0, u.cols, xr, lane);
     else
       load_xm<MT>(a, u.j0, u.cols, xrm, lane);  // (several rows: with the map, like one row)
-    const u32x16 rows2 = unit_rows(mat, unit);
+    const u32x16 rows2 = NW == 16 ? unit_rows_vec(mat, unit) : unit_rows(mat, unit);
     const u32x4 erow = rows2.s0123, own = rows2.s89ab - rows2.s0123;
     // (the class sections' offsets come from the kernel-argument block: read
     // them only after the loads above are issued)
@@ -1620,7 +1635,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) vo
     if (setup_prio) __builtin_amdgcn_s_setprio(1);
     const int wb = (cb * R) >> 6, we = (ce * R + 63) >> 6;
     const WmapRegs wr = load_wmap(mat, u, we, lane);
-    const u32x16 rows2 = unit_rows(mat, unit);  // beside the width map, not after it
+    const u32x16 rows2 = unit_rows_vec(mat, unit);  // beside the width map, not after it
     const uint32_t es[4] = {rows2.s0, rows2.s1, rows2.s2, rows2.s3};
     // values from the kernel-argument block only after the loads above are
     // issued (the compiler would otherwise hoist them and wait for the block)
